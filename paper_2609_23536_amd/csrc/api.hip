@@ -1,0 +1,722 @@
+// C ABI of the FP8 split linear: argument validation, the stage context, the
+// stream-ordered executor with HIP-graph capture / replay, and the stateless
+// hot-path entry points.
+//
+// Executor (§4.4 of the paper): every layer action runs on one context-owned
+// graph stream.  The graph stream first waits on the caller's stream; the
+// action's kernel sequence is then either launched directly (eager) or
+// replayed from a graph captured once per (layer, action, slot); finally an
+// event recorded at the tail is waited on by the caller's stream (the two-way
+// handoff of §2.3).  Captured graphs bind the caller's buffers directly: when
+// an action is called with different pointers or sizes than at capture time,
+// its graph is captured again (counted in qe_ctx_state.captures), so no
+// dynamic-input copy is ever needed.
+#include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <chrono>
+#include <map>
+#include <vector>
+
+#include "../../include/qe.h"
+#include "contract.h"
+#include "kernels.h"
+
+namespace {
+
+int64_t rup16(int64_t v) { return (v + 15) / 16 * 16; }
+
+struct Call {
+  int32_t kind;  // qe::KernelClass
+  int32_t pad;
+  union {
+    qe::QuantParams q;
+    qe::UpdateParams u;
+    qe::GemmParams g;
+  };
+  Call() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
+};
+using Plan = std::vector<Call>;
+
+bool same_plan(const Plan &a, const Plan &b) {
+  return a.size() == b.size() && (a.empty() || memcmp(a.data(), b.data(), a.size() * sizeof(Call)) == 0);
+}
+
+struct SlotDev {
+  uint8_t *x_q_t = nullptr;   // [K, ld_t]
+  uint8_t *dy_q_t = nullptr;  // [N, ld_t]
+  float *x_sinv = nullptr;
+  float *dy_sinv = nullptr;
+};
+
+struct LayerDev {
+  qe_layer_desc desc{};
+  float *meta = nullptr;  // hist[3][H] | scale[3] | scale_inv[3]
+  uint8_t *w_q = nullptr, *w_q_t = nullptr;
+  float *w_sinv = nullptr;
+  uint8_t *x_q = nullptr, *dy_q = nullptr;  // row-wise scratch
+  int64_t ld_wq = 0, ld_wqt = 0, ld_xq = 0, ld_dyq = 0, ld_t = 0;
+  std::vector<SlotDev> slots;
+  std::vector<void *> allocs;
+
+  qe::MetaRef role(int r) const {
+    const int H = desc.history_len;
+    qe::MetaRef m{};
+    m.hist = meta + size_t(r) * H;
+    m.scale = meta + size_t(3) * H + r;
+    m.scale_inv = meta + size_t(3) * H + 3 + r;
+    m.history_len = H;
+    m.margin = desc.margin;
+    m.fmt = r == QE_ROLE_X ? desc.fmt_x : (r == QE_ROLE_W ? desc.fmt_w : desc.fmt_dy);
+    return m;
+  }
+};
+
+struct GraphEntry {
+  hipGraphExec_t exec = nullptr;
+  Plan plan;
+};
+
+struct TimedCall {
+  int kind;
+  hipEvent_t t0, t1;
+};
+
+}  // namespace
+
+struct qe_ctx {
+  qe_config cfg{};
+  qe::Contract contract;
+  hipStream_t gs = nullptr;
+  hipEvent_t ev_in = nullptr, ev_tail = nullptr;
+  long long *d_token = nullptr;
+  std::vector<LayerDev> layers;
+  std::map<uint64_t, GraphEntry> graphs;
+  qe_ctx_state st{};
+  int timing = 0;
+  std::vector<TimedCall> timed;
+  std::vector<hipEvent_t> event_pool;
+  double kc_ms[qe::KC_COUNT] = {0, 0, 0};
+  int64_t kc_n[qe::KC_COUNT] = {0, 0, 0};
+  explicit qe_ctx(const qe_config &c) : cfg(c), contract(c.microbatches) {}
+};
+
+namespace {
+
+bool valid_dtype(int d) { return d == QE_F32 || d == QE_BF16; }
+bool valid_fmt(int f) { return f == QE_E4M3 || f == QE_E5M2; }
+
+hipError_t launch(const Call &c, hipStream_t s) {
+  switch (c.kind) {
+    case qe::KC_QUANT: return qe::launch_quantize(c.q, s);
+    case qe::KC_UPDATE: return qe::launch_scale_update(c.u, s);
+    default: return qe::launch_gemm(c.g, s);
+  }
+}
+
+hipEvent_t pooled_event(qe_ctx *c) {
+  if (!c->event_pool.empty()) {
+    hipEvent_t e = c->event_pool.back();
+    c->event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed) {
+  for (const Call &call : plan) {
+    if (timed) {
+      TimedCall t{call.kind, pooled_event(c), pooled_event(c)};
+      if (!t.t0 || !t.t1) return hipErrorOutOfMemory;
+      hipError_t e = hipEventRecord(t.t0, c->gs);
+      if (e != hipSuccess) return e;
+      e = launch(call, c->gs);
+      if (e != hipSuccess) return e;
+      e = hipEventRecord(t.t1, c->gs);
+      if (e != hipSuccess) return e;
+      c->timed.push_back(t);
+    } else {
+      const hipError_t e = launch(call, c->gs);
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+// Two-way handoff around one action (§2.3, §4.4).
+qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller) {
+  if (caller != c->gs) {
+    if (hipEventRecord(c->ev_in, caller) != hipSuccess) return QE_ERR_HIP;
+    if (hipStreamWaitEvent(c->gs, c->ev_in, 0) != hipSuccess) return QE_ERR_HIP;
+  }
+  if (c->cfg.use_graphs) {
+    GraphEntry &e = c->graphs[gkey];
+    if (e.exec == nullptr || !same_plan(e.plan, plan)) {
+      const auto t0 = std::chrono::steady_clock::now();
+      if (e.exec != nullptr) {
+        (void)hipGraphExecDestroy(e.exec);
+        e.exec = nullptr;
+      }
+      hipGraph_t graph = nullptr;
+      if (hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal) != hipSuccess) return QE_ERR_HIP;
+      const hipError_t le = enqueue(c, plan, false);
+      const hipError_t ce = hipStreamEndCapture(c->gs, &graph);
+      if (le != hipSuccess || ce != hipSuccess || graph == nullptr) {
+        if (graph) (void)hipGraphDestroy(graph);
+        return QE_ERR_HIP;
+      }
+      const hipError_t ie = hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (ie != hipSuccess) {
+        e.exec = nullptr;
+        return QE_ERR_HIP;
+      }
+      e.plan = plan;
+      c->st.captures += 1;
+      c->st.capture_ns +=
+          std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
+    }
+    if (hipGraphLaunch(e.exec, c->gs) != hipSuccess) return QE_ERR_HIP;
+    c->st.replays += 1;
+  } else {
+    if (enqueue(c, plan, c->timing != 0) != hipSuccess) return QE_ERR_HIP;
+  }
+  if (hipEventRecord(c->ev_tail, c->gs) != hipSuccess) return QE_ERR_HIP;
+  if (!c->cfg.one_way_handoff && caller != c->gs) {
+    if (hipStreamWaitEvent(caller, c->ev_tail, 0) != hipSuccess) return QE_ERR_HIP;
+  }
+  c->st.handoffs += 2;
+  return QE_OK;
+}
+
+uint64_t graph_key(int layer, int action, uint32_t slot) {
+  return (uint64_t(uint32_t(layer)) << 32) | (uint64_t(action) << 24) | uint64_t(slot);
+}
+enum { ACT_FWD = 1, ACT_FWD_REFRESH = 2, ACT_DGRAD = 3, ACT_WGRAD = 4, ACT_FULL = 5 };
+
+Call quant_call(const void *in, int in_dt, int64_t rows, int64_t cols, const qe::MetaRef &m, uint8_t *q_row,
+                int64_t ld_row, uint8_t *q_col, int64_t ld_col, float *snapshot) {
+  Call c;
+  c.kind = qe::KC_QUANT;
+  c.q.in = in;
+  c.q.in_bf16 = in_dt == QE_BF16;
+  c.q.fmt = m.fmt;
+  c.q.rows = rows;
+  c.q.cols = cols;
+  c.q.scale = m.scale;
+  c.q.scale_inv = m.scale_inv;
+  c.q.amax_slot = m.hist;
+  c.q.q_row = q_row;
+  c.q.ld_row = ld_row;
+  c.q.q_col = q_col;
+  c.q.ld_col = ld_col;
+  c.q.snapshot = snapshot;
+  return c;
+}
+
+Call gemm_call(const uint8_t *a, int fa, int64_t lda, const uint8_t *b, int fb, int64_t ldb, int64_t m, int64_t n,
+               int64_t k, const float *sa, const float *sb, void *cptr, int c_dt, int64_t ldc, int mode) {
+  Call c;
+  c.kind = qe::KC_GEMM;
+  c.g.a = a;
+  c.g.b = b;
+  c.g.lda = lda;
+  c.g.ldb = ldb;
+  c.g.m = m;
+  c.g.n = n;
+  c.g.k = k;
+  c.g.a_scale_inv = sa;
+  c.g.b_scale_inv = sb;
+  c.g.c = cptr;
+  c.g.ldc = ldc;
+  c.g.fmt_a = fa;
+  c.g.fmt_b = fb;
+  c.g.out = mode == QE_PLACE_ACCUM ? 2 : (c_dt == QE_BF16 ? 1 : 0);
+  return c;
+}
+
+Call update_call(const LayerDev &L, std::initializer_list<int> roles, long long *token) {
+  Call c;
+  c.kind = qe::KC_UPDATE;
+  int n = 0;
+  for (int r : roles) c.u.m[n++] = L.role(r);
+  c.u.n = n;
+  c.u.token = token;
+  return c;
+}
+
+// Plans of the physical actions (the kernel sequences of §3.2).
+Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt, int64_t tokens, void *y, int y_dt,
+              bool refresh) {
+  const qe_layer_desc &d = L.desc;
+  const SlotDev &S = L.slots[m];
+  Plan p;
+  if (refresh)
+    p.push_back(quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt,
+                           L.w_sinv));
+  p.push_back(quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv));
+  p.push_back(gemm_call(L.x_q, d.fmt_x, L.ld_xq, L.w_q, d.fmt_w, L.ld_wq, tokens, d.n_out, d.k_in, S.x_sinv, L.w_sinv,
+                        y, y_dt, d.n_out, QE_PLACE_INIT));
+  p.push_back(update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token));
+  return p;
+}
+
+void append_dgrad(qe_ctx *c, Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, const void *dy, int dy_dt,
+                  void *dx, int dx_dt) {
+  (void)c;
+  const qe_layer_desc &d = L.desc;
+  const SlotDev &S = L.slots[m];
+  p.push_back(quant_call(dy, dy_dt, tokens, d.n_out, L.role(QE_ROLE_DY), L.dy_q, L.ld_dyq, S.dy_q_t, L.ld_t,
+                         S.dy_sinv));
+  p.push_back(gemm_call(L.dy_q, d.fmt_dy, L.ld_dyq, L.w_q_t, d.fmt_w, L.ld_wqt, tokens, d.k_in, d.n_out, S.dy_sinv,
+                        L.w_sinv, dx, dx_dt, d.k_in, QE_PLACE_INIT));
+}
+
+void append_wgrad(Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, float *mg, int64_t offset, int64_t ld,
+                  int mode) {
+  const qe_layer_desc &d = L.desc;
+  const SlotDev &S = L.slots[m];
+  p.push_back(gemm_call(S.dy_q_t, d.fmt_dy, L.ld_t, S.x_q_t, d.fmt_x, L.ld_t, d.n_out, d.k_in, tokens, S.dy_sinv,
+                        S.x_sinv, mg + offset, QE_F32, ld, mode));
+}
+
+qe_status fail_physical(qe_ctx *c) {
+  c->contract.abort_epoch();
+  return QE_ERR_HIP;
+}
+
+void *dev_alloc(qe_ctx *c, LayerDev &L, size_t bytes, bool *ok) {
+  void *p = nullptr;
+  if (bytes == 0) bytes = 16;
+  if (hipMalloc(&p, bytes) != hipSuccess) {
+    *ok = false;
+    return nullptr;
+  }
+  if (hipMemset(p, 0, bytes) != hipSuccess) *ok = false;
+  L.allocs.push_back(p);
+  c->st.device_bytes += int64_t(bytes);
+  return p;
+}
+
+bool meta_ok(const qe_fp8_meta *m) {
+  return m && m->amax_history && m->scale && m->scale_inv && m->history_len >= 1 &&
+         m->history_len <= qe::kMaxHistory && valid_fmt(m->fmt);
+}
+
+qe::MetaRef meta_ref(const qe_fp8_meta &m) {
+  qe::MetaRef r{};
+  r.hist = m.amax_history;
+  r.scale = m.scale;
+  r.scale_inv = m.scale_inv;
+  r.history_len = m.history_len;
+  r.margin = m.margin;
+  r.fmt = m.fmt;
+  return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *qe_status_str(qe_status s) {
+  switch (s) {
+    case QE_OK: return "OK";
+    case QE_ERR_INVALID_ARG: return "INVALID_ARG";
+    case QE_ERR_STALE_REF: return "STALE_REF";
+    case QE_ERR_KEY_MISMATCH: return "KEY_MISMATCH";
+    case QE_ERR_KEY_LIVE: return "KEY_LIVE";
+    case QE_ERR_POOL_FULL: return "POOL_FULL";
+    case QE_ERR_DUPLICATE_CONSUMER: return "DUPLICATE_CONSUMER";
+    case QE_ERR_ORDER: return "ORDER";
+    case QE_ERR_EPOCH: return "EPOCH";
+    case QE_ERR_STALE_CACHE: return "STALE_CACHE";
+    case QE_ERR_DEST_MISMATCH: return "DEST_MISMATCH";
+    case QE_ERR_DEST_ALIAS: return "DEST_ALIAS";
+    case QE_ERR_DUP_WRITE: return "DUP_WRITE";
+    case QE_ERR_ARENA_INVALID: return "ARENA_INVALID";
+    case QE_ERR_INCOMPLETE: return "INCOMPLETE";
+    case QE_ERR_NOT_QUIESCENT: return "NOT_QUIESCENT";
+    case QE_ERR_HIP: return "HIP";
+    case QE_ERR_UNSUPPORTED: return "UNSUPPORTED";
+  }
+  return "UNKNOWN";
+}
+
+// ------------------------------------------------------------------ stateless hot-path calls
+qe_status qe_amax_scale_update(const qe_fp8_meta *metas_host, int32_t n_metas, int64_t *device_token,
+                               qe_stream stream) {
+  if (metas_host == nullptr || n_metas < 1 || n_metas > qe::kMaxMetas) return QE_ERR_INVALID_ARG;
+  qe::UpdateParams p;
+  memset(&p, 0, sizeof(p));
+  for (int i = 0; i < n_metas; ++i) {
+    if (!meta_ok(&metas_host[i])) return QE_ERR_INVALID_ARG;
+    p.m[i] = meta_ref(metas_host[i]);
+  }
+  p.n = n_metas;
+  p.token = reinterpret_cast<long long *>(device_token);
+  return qe::launch_scale_update(p, static_cast<hipStream_t>(stream)) == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+qe_status qe_quantize_fp8(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols, const qe_fp8_meta *meta_host,
+                          uint8_t *q_row, int64_t ld_row, uint8_t *q_col, int64_t ld_col, float *scale_inv_snapshot,
+                          qe_stream stream) {
+  if (!valid_dtype(in_dtype) || rows < 0 || cols < 0 || !meta_ok(meta_host)) return QE_ERR_INVALID_ARG;
+  if (rows > 0 && cols > 0 && in == nullptr) return QE_ERR_INVALID_ARG;
+  if (q_row != nullptr && ld_row < cols) return QE_ERR_INVALID_ARG;
+  if (q_col != nullptr && ld_col < rows) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(in) % (in_dtype == QE_BF16 ? 2 : 4) != 0) return QE_ERR_INVALID_ARG;
+  const qe::MetaRef m = meta_ref(*meta_host);
+  const Call c = quant_call(in, in_dtype, rows, cols, m, q_row, ld_row, q_col, ld_col, scale_inv_snapshot);
+  return qe::launch_quantize(c.q, static_cast<hipStream_t>(stream)) == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const uint8_t *b, qe_fp8_fmt fmt_b,
+                         int64_t ldb, int64_t m, int64_t n, int64_t k, const float *a_scale_inv,
+                         const float *b_scale_inv, void *c, qe_dtype c_dtype, int64_t ldc, qe_place_mode mode,
+                         qe_stream stream) {
+  if (!valid_fmt(fmt_a) || !valid_fmt(fmt_b) || !valid_dtype(c_dtype)) return QE_ERR_INVALID_ARG;
+  if (mode != QE_PLACE_INIT && mode != QE_PLACE_ACCUM) return QE_ERR_INVALID_ARG;
+  if (mode == QE_PLACE_ACCUM && c_dtype != QE_F32) return QE_ERR_INVALID_ARG;
+  if (m < 0 || n < 0 || k < 0 || ldc < n) return QE_ERR_INVALID_ARG;
+  if (m == 0 || n == 0) return QE_OK;
+  if (!a || !b || !c || !a_scale_inv || !b_scale_inv) return QE_ERR_INVALID_ARG;
+  if (lda % 16 || ldb % 16 || lda < rup16(k) || ldb < rup16(k)) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(a) % 16 || uintptr_t(b) % 16) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(c) % (c_dtype == QE_F32 ? 4 : 2)) return QE_ERR_INVALID_ARG;
+  const Call call = gemm_call(a, fmt_a, lda, b, fmt_b, ldb, m, n, k, a_scale_inv, b_scale_inv, c, c_dtype, ldc, mode);
+  return qe::launch_gemm(call.g, static_cast<hipStream_t>(stream)) == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+// ------------------------------------------------------------------ context
+qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
+  if (cfg_host == nullptr || out_host == nullptr || cfg_host->microbatches < 1 || cfg_host->microbatches > 4096)
+    return QE_ERR_INVALID_ARG;
+  *out_host = nullptr;
+  qe_ctx *c = new qe_ctx(*cfg_host);
+  c->st.device_token = -1;
+  c->st.arena_valid = 1;
+  if (!c->cfg.null_executor) {
+    hipDeviceProp_t prop;
+    if (hipSetDevice(c->cfg.device) != hipSuccess || hipGetDeviceProperties(&prop, c->cfg.device) != hipSuccess) {
+      delete c;
+      return QE_ERR_HIP;
+    }
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+      delete c;
+      return QE_ERR_UNSUPPORTED;
+    }
+    bool ok = hipStreamCreateWithFlags(&c->gs, hipStreamNonBlocking) == hipSuccess;
+    ok = ok && hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming) == hipSuccess;
+    ok = ok && hipEventCreateWithFlags(&c->ev_tail, hipEventDisableTiming) == hipSuccess;
+    ok = ok && hipMalloc(reinterpret_cast<void **>(&c->d_token), sizeof(long long)) == hipSuccess;
+    ok = ok && hipMemset(c->d_token, 0, sizeof(long long)) == hipSuccess;
+    if (!ok) {
+      qe_ctx_destroy(c);
+      return QE_ERR_HIP;
+    }
+  }
+  *out_host = c;
+  return QE_OK;
+}
+
+void qe_ctx_destroy(qe_ctx *c) {
+  if (c == nullptr) return;
+  if (!c->cfg.null_executor) {
+    if (c->gs) (void)hipStreamSynchronize(c->gs);
+    for (auto &kv : c->graphs)
+      if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
+    for (auto &L : c->layers)
+      for (void *p : L.allocs) (void)hipFree(p);
+    for (auto &t : c->timed) {
+      (void)hipEventDestroy(t.t0);
+      (void)hipEventDestroy(t.t1);
+    }
+    for (hipEvent_t e : c->event_pool) (void)hipEventDestroy(e);
+    if (c->d_token) (void)hipFree(c->d_token);
+    if (c->ev_in) (void)hipEventDestroy(c->ev_in);
+    if (c->ev_tail) (void)hipEventDestroy(c->ev_tail);
+    if (c->gs) (void)hipStreamDestroy(c->gs);
+  }
+  delete c;
+}
+
+qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_out_host) {
+  if (c == nullptr || d == nullptr || layer_out_host == nullptr) return QE_ERR_INVALID_ARG;
+  if (d->n_out < 1 || d->k_in < 1 || d->max_tokens < 0 || d->history_len < 1 || d->history_len > qe::kMaxHistory ||
+      d->margin < -126 || d->margin > 252 || !valid_dtype(d->w_dtype) || !valid_fmt(d->fmt_x) ||
+      !valid_fmt(d->fmt_w) || !valid_fmt(d->fmt_dy))
+    return QE_ERR_INVALID_ARG;
+  if (!c->cfg.null_executor && d->w == nullptr) return QE_ERR_INVALID_ARG;
+  if (c->contract.has_layer(d->stage, d->unit)) return QE_ERR_INVALID_ARG;
+  LayerDev L;
+  L.desc = *d;
+  const int M = c->cfg.microbatches;
+  L.slots.resize(size_t(M));
+  L.ld_wq = rup16(d->k_in);
+  L.ld_wqt = rup16(d->n_out);
+  L.ld_xq = rup16(d->k_in);
+  L.ld_dyq = rup16(d->n_out);
+  L.ld_t = rup16(d->max_tokens);
+  if (!c->cfg.null_executor) {
+    bool ok = true;
+    const int H = d->history_len;
+    L.meta = static_cast<float *>(dev_alloc(c, L, sizeof(float) * (3 * size_t(H) + 6), &ok));
+    L.w_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->n_out) * L.ld_wq, &ok));
+    L.w_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->k_in) * L.ld_wqt, &ok));
+    L.w_sinv = static_cast<float *>(dev_alloc(c, L, sizeof(float), &ok));
+    L.x_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->max_tokens) * L.ld_xq, &ok));
+    L.dy_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->max_tokens) * L.ld_dyq, &ok));
+    for (auto &S : L.slots) {
+      S.x_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->k_in) * L.ld_t, &ok));
+      S.dy_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->n_out) * L.ld_t, &ok));
+      S.x_sinv = static_cast<float *>(dev_alloc(c, L, sizeof(float), &ok));
+      S.dy_sinv = static_cast<float *>(dev_alloc(c, L, sizeof(float), &ok));
+    }
+    if (ok) {
+      const float ones[6] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
+      ok = hipMemcpy(L.meta + 3 * size_t(H), ones, sizeof(ones), hipMemcpyHostToDevice) == hipSuccess;
+      ok = ok && hipMemcpy(L.w_sinv, ones, sizeof(float), hipMemcpyHostToDevice) == hipSuccess;
+    }
+    if (!ok) {
+      for (void *p : L.allocs) (void)hipFree(p);
+      return QE_ERR_HIP;
+    }
+  }
+  *layer_out_host = c->contract.add_layer(d->stage, d->unit, d->n_out, d->k_in, d->max_tokens);
+  c->layers.push_back(L);
+  return QE_OK;
+}
+
+qe_status qe_layer_meta(const qe_ctx *c, int32_t layer, qe_role role, qe_fp8_meta *out) {
+  if (c == nullptr || out == nullptr || layer < 0 || layer >= int(c->layers.size()) || role < 0 || role > 2)
+    return QE_ERR_INVALID_ARG;
+  const LayerDev &L = c->layers[size_t(layer)];
+  memset(out, 0, sizeof(*out));
+  out->history_len = L.desc.history_len;
+  out->margin = L.desc.margin;
+  out->fmt = role == QE_ROLE_X ? L.desc.fmt_x : (role == QE_ROLE_W ? L.desc.fmt_w : L.desc.fmt_dy);
+  if (L.meta != nullptr) {
+    const qe::MetaRef m = L.role(role);
+    out->amax_history = m.hist;
+    out->scale = m.scale;
+    out->scale_inv = m.scale_inv;
+  }
+  return QE_OK;
+}
+
+qe_status qe_layer_cache(const qe_ctx *c, int32_t layer, const uint8_t **w_q, int64_t *ld_w_q, const uint8_t **w_q_t,
+                         int64_t *ld_w_q_t, const float **w_scale_inv) {
+  if (c == nullptr || layer < 0 || layer >= int(c->layers.size())) return QE_ERR_INVALID_ARG;
+  const LayerDev &L = c->layers[size_t(layer)];
+  if (w_q) *w_q = L.w_q;
+  if (ld_w_q) *ld_w_q = L.ld_wq;
+  if (w_q_t) *w_q_t = L.w_q_t;
+  if (ld_w_q_t) *ld_w_q_t = L.ld_wqt;
+  if (w_scale_inv) *w_scale_inv = L.w_sinv;
+  return QE_OK;
+}
+
+qe_status qe_layer_slot_payload(const qe_ctx *c, int32_t layer, int32_t slot, const uint8_t **x_q_t,
+                                int64_t *ld_x_q_t, const uint8_t **dy_q_t, int64_t *ld_dy_q_t,
+                                const float **x_scale_inv, const float **dy_scale_inv) {
+  if (c == nullptr || layer < 0 || layer >= int(c->layers.size()) || slot < 0 || slot >= c->cfg.microbatches)
+    return QE_ERR_INVALID_ARG;
+  const LayerDev &L = c->layers[size_t(layer)];
+  const SlotDev &S = L.slots[size_t(slot)];
+  if (x_q_t) *x_q_t = S.x_q_t;
+  if (ld_x_q_t) *ld_x_q_t = L.ld_t;
+  if (dy_q_t) *dy_q_t = S.dy_q_t;
+  if (ld_dy_q_t) *ld_dy_q_t = L.ld_t;
+  if (x_scale_inv) *x_scale_inv = S.x_sinv;
+  if (dy_scale_inv) *dy_scale_inv = S.dy_sinv;
+  return QE_OK;
+}
+
+// ------------------------------------------------------------------ actions
+qe_status qe_fp8_linear_fwd(qe_ctx *c, int32_t layer, qe_tape_key key, const void *x, qe_dtype x_dtype,
+                            int64_t tokens, void *y, qe_dtype y_dtype, qe_tape_ref *ref_out_host, qe_stream caller) {
+  if (c == nullptr || ref_out_host == nullptr || !valid_dtype(x_dtype) || !valid_dtype(y_dtype))
+    return QE_ERR_INVALID_ARG;
+  if (!c->cfg.null_executor && tokens > 0 && (x == nullptr || y == nullptr)) return QE_ERR_INVALID_ARG;
+  bool refresh = false;
+  const qe_status st = c->contract.check_fwd(layer, key, tokens, &refresh);
+  if (st != QE_OK) return st;
+  if (c->contract.physical_fails()) return fail_physical(c);
+  if (!c->cfg.null_executor) {
+    const LayerDev &L = c->layers[size_t(layer)];
+    const Plan p = plan_fwd(c, L, key.microbatch, x, x_dtype, tokens, y, y_dtype, refresh);
+    if (run_plan(c, p, graph_key(layer, refresh ? ACT_FWD_REFRESH : ACT_FWD, key.microbatch),
+                 static_cast<hipStream_t>(caller)) != QE_OK)
+      return fail_physical(c);
+  }
+  *ref_out_host = c->contract.commit_fwd(layer, key, tokens, refresh);
+  return QE_OK;
+}
+
+qe_status qe_fp8_linear_dgrad(qe_ctx *c, int32_t layer, qe_tape_key key, qe_tape_ref ref, const void *dy,
+                              qe_dtype dy_dtype, void *dx, qe_dtype dx_dtype, qe_stream caller) {
+  if (c == nullptr || !valid_dtype(dy_dtype) || !valid_dtype(dx_dtype)) return QE_ERR_INVALID_ARG;
+  const qe_status st = c->contract.check_dgrad(layer, key, ref);
+  if (st != QE_OK) return st;
+  const int64_t tokens = c->contract.layer(layer).slots[ref.slot].tokens;
+  if (!c->cfg.null_executor && tokens > 0 && (dy == nullptr || dx == nullptr)) return QE_ERR_INVALID_ARG;
+  if (c->contract.physical_fails()) return fail_physical(c);
+  if (!c->cfg.null_executor) {
+    const LayerDev &L = c->layers[size_t(layer)];
+    Plan p;
+    append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
+    p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+    if (run_plan(c, p, graph_key(layer, ACT_DGRAD, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
+      return fail_physical(c);
+  }
+  c->contract.commit_dgrad(layer, ref);
+  return QE_OK;
+}
+
+qe_status qe_fp8_linear_wgrad_place(qe_ctx *c, int32_t layer, qe_tape_key key, qe_tape_ref ref, float *main_grad,
+                                    int64_t offset, int64_t ld, qe_place_mode mode, qe_stream caller) {
+  if (c == nullptr) return QE_ERR_INVALID_ARG;
+  const qe_status st =
+      c->contract.check_wgrad(layer, key, ref, reinterpret_cast<uintptr_t>(main_grad), offset, ld, int(mode));
+  if (st != QE_OK) return st;
+  if (c->contract.physical_fails()) return fail_physical(c);
+  if (!c->cfg.null_executor) {
+    const LayerDev &L = c->layers[size_t(layer)];
+    const int64_t tokens = c->contract.layer(layer).slots[ref.slot].tokens;
+    Plan p;
+    append_wgrad(p, L, ref.slot, tokens, main_grad, offset, ld, mode);
+    if (run_plan(c, p, graph_key(layer, ACT_WGRAD, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
+      return fail_physical(c);
+  }
+  c->contract.commit_wgrad(layer, ref);
+  return QE_OK;
+}
+
+qe_status qe_fp8_linear_bwd_full(qe_ctx *c, int32_t layer, qe_tape_key key, qe_tape_ref ref, const void *dy,
+                                 qe_dtype dy_dtype, void *dx, qe_dtype dx_dtype, float *main_grad, int64_t offset,
+                                 int64_t ld, qe_place_mode mode, qe_stream caller) {
+  if (c == nullptr || !valid_dtype(dy_dtype) || !valid_dtype(dx_dtype)) return QE_ERR_INVALID_ARG;
+  const qe_status st =
+      c->contract.check_bwd_full(layer, key, ref, reinterpret_cast<uintptr_t>(main_grad), offset, ld, int(mode));
+  if (st != QE_OK) return st;
+  const int64_t tokens = c->contract.layer(layer).slots[ref.slot].tokens;
+  if (!c->cfg.null_executor && tokens > 0 && (dy == nullptr || dx == nullptr)) return QE_ERR_INVALID_ARG;
+  if (c->contract.physical_fails()) return fail_physical(c);
+  if (!c->cfg.null_executor) {
+    const LayerDev &L = c->layers[size_t(layer)];
+    Plan p;
+    append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
+    append_wgrad(p, L, ref.slot, tokens, main_grad, offset, ld, mode);
+    p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+    if (run_plan(c, p, graph_key(layer, ACT_FULL, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
+      return fail_physical(c);
+  }
+  c->contract.commit_bwd_full(layer, ref);
+  return QE_OK;
+}
+
+// ------------------------------------------------------------------ arena / epoch
+qe_status qe_arena_bind(qe_ctx *c, int32_t layer, uint32_t microbatch, float *buf, int64_t buf_elems, int64_t offset,
+                        int64_t ld) {
+  if (c == nullptr) return QE_ERR_INVALID_ARG;
+  return c->contract.bind(layer, int64_t(microbatch), reinterpret_cast<uintptr_t>(buf), buf_elems, offset, ld);
+}
+
+qe_status qe_arena_finalize(qe_ctx *c) { return c ? c->contract.finalize() : QE_ERR_INVALID_ARG; }
+qe_status qe_optimizer_commit(qe_ctx *c) { return c ? c->contract.optimizer_commit() : QE_ERR_INVALID_ARG; }
+qe_status qe_arena_rebuild(qe_ctx *c) { return c ? c->contract.rebuild() : QE_ERR_INVALID_ARG; }
+
+qe_status qe_abort_epoch(qe_ctx *c) {
+  if (c == nullptr) return QE_ERR_INVALID_ARG;
+  c->contract.abort_epoch();
+  return QE_OK;
+}
+
+qe_status qe_sync(qe_ctx *c) {
+  if (c == nullptr) return QE_ERR_INVALID_ARG;
+  if (c->cfg.null_executor) return QE_OK;
+  if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+  long long tok = 0;
+  if (hipMemcpy(&tok, c->d_token, sizeof(tok), hipMemcpyDeviceToHost) != hipSuccess) return QE_ERR_HIP;
+  c->st.device_token = tok;
+  return QE_OK;
+}
+
+qe_status qe_get_state(const qe_ctx *c, qe_ctx_state *out) {
+  if (c == nullptr || out == nullptr) return QE_ERR_INVALID_ARG;
+  *out = c->st;
+  out->e_w = c->contract.e_w();
+  out->token = c->contract.token();
+  out->arena_valid = c->contract.arena_valid();
+  out->finalized = c->contract.finalized();
+  out->graphs = int64_t(c->graphs.size());
+  out->arena_bytes = c->contract.arena_bytes();
+  return QE_OK;
+}
+
+qe_status qe_get_layer_state(const qe_ctx *c, int32_t layer, qe_layer_state *out) {
+  if (c == nullptr || out == nullptr || layer < 0 || layer >= c->contract.num_layers()) return QE_ERR_INVALID_ARG;
+  const qe::LayerBook &L = c->contract.layer(layer);
+  memset(out, 0, sizeof(*out));
+  out->e_c = L.e_c;
+  out->refreshes = L.refreshes;
+  out->n_slots = int32_t(L.slots.size());
+  return QE_OK;
+}
+
+qe_status qe_get_slot_state(const qe_ctx *c, int32_t layer, int32_t slot, qe_slot_state *out) {
+  if (c == nullptr || out == nullptr || layer < 0 || layer >= c->contract.num_layers() || slot < 0 ||
+      slot >= c->cfg.microbatches)
+    return QE_ERR_INVALID_ARG;
+  const qe::LayerBook &L = c->contract.layer(layer);
+  const qe::SlotState &S = L.slots[size_t(slot)];
+  const qe::View &V = L.views[size_t(slot)];
+  memset(out, 0, sizeof(*out));
+  out->live = S.live;
+  out->generation = S.generation;
+  out->bits = S.bits;
+  out->key = S.key;
+  out->tokens = S.tokens;
+  out->bound = V.bound;
+  out->written = V.written;
+  out->view_offset = V.offset;
+  out->view_ld = V.ld;
+  out->view_buf = reinterpret_cast<const float *>(V.buf);
+  return QE_OK;
+}
+
+qe_status qe_inject_fault(qe_ctx *c, int32_t n) {
+  if (c == nullptr || n < 0) return QE_ERR_INVALID_ARG;
+  c->contract.inject_fault(n);
+  return QE_OK;
+}
+
+qe_status qe_set_kernel_timing(qe_ctx *c, int32_t enable) {
+  if (c == nullptr) return QE_ERR_INVALID_ARG;
+  c->timing = enable != 0;
+  return QE_OK;
+}
+
+qe_status qe_get_kernel_timing(qe_ctx *c, int32_t kernel_class, double *total_ms_host, int64_t *launches_host) {
+  if (c == nullptr || kernel_class < 0 || kernel_class >= qe::KC_COUNT || !total_ms_host || !launches_host)
+    return QE_ERR_INVALID_ARG;
+  if (!c->cfg.null_executor && !c->timed.empty()) {
+    if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    for (auto &t : c->timed) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, t.t0, t.t1) != hipSuccess) return QE_ERR_HIP;
+      c->kc_ms[t.kind] += ms;
+      c->kc_n[t.kind] += 1;
+      c->event_pool.push_back(t.t0);
+      c->event_pool.push_back(t.t1);
+    }
+    c->timed.clear();
+  }
+  *total_ms_host = c->kc_ms[kernel_class];
+  *launches_host = c->kc_n[kernel_class];
+  return QE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,243 @@
+// FP8 quantization with fused transpose and amax recording (gfx950).
+//
+// Delayed scaling (§2.1 of the paper): a tensor is cast with the scale the
+// previous update produced, and its amax is recorded for later updates.  The
+// split backward (§3.2) needs each operand both row-wise (for F / dI) and
+// column-wise (for the deferred dW), so one pass writes both:
+//   q_row[r][c] = Q(x[r][c] * scale),  q_col[c][r] = the same code,
+//   history[0]  = max(history[0], max |x|)      (unscaled, NaN propagates)
+// Q rounds to nearest even and saturates to +-fmax; NaN becomes 0x7F with the
+// input's sign bit.  Formats: OCP E4M3 (max 448) and E5M2 (max 57344).
+//
+// Layout: one workgroup of 256 lanes per 128 x 128 tile.  Phase 1: eight lanes
+// cover one 128-element row segment with 16-byte loads (bf16: 2, fp32: 4 per
+// lane), convert 16 values to one 16-byte code vector, store it row-wise and
+// into an LDS tile whose 16-byte chunks are XOR-swizzled by row block.
+// Phase 2: each lane gathers a 16-row x 4-column block of codes from LDS and
+// writes four 16-byte column segments; eight consecutive lanes complete one
+// 128-byte run of a transposed row.  amax: a max over the |x| bit patterns
+// (which order like the values, NaN above inf) per lane, a wave shuffle
+// reduction, then one atomicMax per workgroup.  HBM-bound: per element it
+// moves 2 or 4 bytes in and 2 bytes out.
+#include "kernels.h"
+
+namespace qe {
+namespace {
+
+constexpr int kTile = 128;
+constexpr int kThreads = 256;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t nan_fix(uint32_t u, int byte, float v) {
+  if (v != v) {
+    uint32_t code = 0x7fu | ((__float_as_uint(v) >> 24) & 0x80u);
+    u = (u & ~(0xffu << (8 * byte))) | (code << (8 * byte));
+  }
+  return u;
+}
+
+// Four scaled values -> four FP8 codes, byte i = value i.
+template <int FMT>
+__device__ __forceinline__ uint32_t enc4(float a, float b, float c, float d) {
+  constexpr float fm = FMT == 0 ? 448.0f : 57344.0f;
+  const float ca = fminf(fmaxf(a, -fm), fm);
+  const float cb = fminf(fmaxf(b, -fm), fm);
+  const float cc = fminf(fmaxf(c, -fm), fm);
+  const float cd = fminf(fmaxf(d, -fm), fm);
+  int r;
+  if constexpr (FMT == 0) {
+    r = __builtin_amdgcn_cvt_pk_fp8_f32(ca, cb, 0, false);
+    r = __builtin_amdgcn_cvt_pk_fp8_f32(cc, cd, r, true);
+  } else {
+    r = __builtin_amdgcn_cvt_pk_bf8_f32(ca, cb, 0, false);
+    r = __builtin_amdgcn_cvt_pk_bf8_f32(cc, cd, r, true);
+  }
+  uint32_t u = uint32_t(r);
+  if (__builtin_expect((a != a) | (b != b) | (c != c) | (d != d), 0)) {
+    u = nan_fix(u, 0, a);
+    u = nan_fix(u, 1, b);
+    u = nan_fix(u, 2, c);
+    u = nan_fix(u, 3, d);
+  }
+  return u;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ uint32_t abs_bits(float v) { return __float_as_uint(v) & 0x7fffffffu; }
+
+// 16 floats -> 16 codes (+ running amax)
+template <int FMT>
+__device__ __forceinline__ uint4 encode16(const float (&f)[16], float scale, uint32_t &amax) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    uint32_t b = abs_bits(f[e]);
+    amax = b > amax ? b : amax;
+  }
+  uint4 q;
+  q.x = enc4<FMT>(f[0] * scale, f[1] * scale, f[2] * scale, f[3] * scale);
+  q.y = enc4<FMT>(f[4] * scale, f[5] * scale, f[6] * scale, f[7] * scale);
+  q.z = enc4<FMT>(f[8] * scale, f[9] * scale, f[10] * scale, f[11] * scale);
+  q.w = enc4<FMT>(f[12] * scale, f[13] * scale, f[14] * scale, f[15] * scale);
+  return q;
+}
+
+__device__ __forceinline__ uint32_t lds_chunk_offset(int row, int chunk) {
+  return uint32_t(row) * kTile + (uint32_t((chunk ^ (row >> 4)) & 7) << 4);
+}
+
+__device__ __forceinline__ uint32_t byte_of(uint32_t w, int j) { return (w >> (8 * j)) & 0xffu; }
+
+template <bool BF16, int FMT>
+__global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64_t tiles_c, int aligned) {
+  __shared__ __attribute__((aligned(16))) uint8_t tile[kTile * kTile];
+  __shared__ uint32_t red[kThreads / 64];
+  constexpr int kVec = BF16 ? 2 : 4;  // 16-byte loads per 16 elements
+  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int64_t r0 = (t / tiles_c) * kTile;
+  const int64_t c0 = (t % tiles_c) * kTile;
+  const float scale = *p.scale;
+  if (t == 0 && tid == 0 && p.snapshot != nullptr) *p.snapshot = *p.scale_inv;
+  const bool full = aligned && r0 + kTile <= p.rows && c0 + kTile <= p.cols;
+  uint32_t amax = 0;
+
+  if (full) {
+    uint4 raw[4][kVec];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int q = it * kThreads + tid, row = q >> 3, cc = q & 7;
+      const int64_t eoff = (r0 + row) * p.cols + c0 + cc * 16;
+      const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const char *>(p.in) + eoff * (BF16 ? 2 : 4));
+#pragma unroll
+      for (int v = 0; v < kVec; ++v) {
+        const u32x4 x = __builtin_nontemporal_load(src + v);
+        raw[it][v] = make_uint4(x.x, x.y, x.z, x.w);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int q = it * kThreads + tid, row = q >> 3, cc = q & 7;
+      float f[16];
+      if constexpr (BF16) {
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+          const uint32_t w[4] = {raw[it][v].x, raw[it][v].y, raw[it][v].z, raw[it][v].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            f[v * 8 + 2 * e] = bf16_to_f32(w[e] & 0xffffu);
+            f[v * 8 + 2 * e + 1] = bf16_to_f32(w[e] >> 16);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          f[4 * v + 0] = __uint_as_float(raw[it][v].x);
+          f[4 * v + 1] = __uint_as_float(raw[it][v].y);
+          f[4 * v + 2] = __uint_as_float(raw[it][v].z);
+          f[4 * v + 3] = __uint_as_float(raw[it][v].w);
+        }
+      }
+      const uint4 codes = encode16<FMT>(f, scale, amax);
+      if (p.q_row != nullptr)
+        *reinterpret_cast<uint4 *>(p.q_row + (r0 + row) * p.ld_row + c0 + cc * 16) = codes;
+      *reinterpret_cast<uint4 *>(tile + lds_chunk_offset(row, cc)) = codes;
+    }
+  } else {
+    for (int it = 0; it < 4; ++it) {
+      const int q = it * kThreads + tid, row = q >> 3, cc = q & 7;
+      const int64_t r = r0 + row;
+      float f[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t c = c0 + cc * 16 + e;
+        float v = 0.0f;
+        if (r < p.rows && c < p.cols) {
+          if constexpr (BF16)
+            v = bf16_to_f32(static_cast<const uint16_t *>(p.in)[r * p.cols + c]);
+          else
+            v = static_cast<const float *>(p.in)[r * p.cols + c];
+        }
+        f[e] = v;
+      }
+      const uint4 codes = encode16<FMT>(f, scale, amax);
+      if (p.q_row != nullptr && r < p.rows) {
+        const uint32_t w[4] = {codes.x, codes.y, codes.z, codes.w};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int64_t c = c0 + cc * 16 + e;
+          if (c < p.cols) p.q_row[r * p.ld_row + c] = uint8_t(byte_of(w[e >> 2], e & 3));
+        }
+      }
+      *reinterpret_cast<uint4 *>(tile + lds_chunk_offset(row, cc)) = codes;
+    }
+  }
+
+  // amax: wave shuffle reduction, then one atomic per workgroup
+  for (int off = 32; off > 0; off >>= 1) {
+    uint32_t o = __shfl_xor(amax, off, 64);
+    amax = o > amax ? o : amax;
+  }
+  if ((tid & 63) == 0) red[tid >> 6] = amax;
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t a = red[0];
+    for (int w = 1; w < kThreads / 64; ++w) a = red[w] > a ? red[w] : a;
+    if (a != 0u) atomicMax(reinterpret_cast<unsigned int *>(p.amax_slot), a);
+  }
+
+  if (p.q_col == nullptr) return;
+  // Phase 2: lane (rb, cq) transposes rows rb*16..+16 x columns 4cq..4cq+3.
+  const int rb = tid & 7, cq = tid >> 3;
+  uint32_t d[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int R = rb * 16 + i;
+    d[i] = *reinterpret_cast<const uint32_t *>(tile + lds_chunk_offset(R, cq >> 2) + ((cq & 3) << 2));
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      w[q] = byte_of(d[4 * q], j) | (byte_of(d[4 * q + 1], j) << 8) | (byte_of(d[4 * q + 2], j) << 16) |
+             (byte_of(d[4 * q + 3], j) << 24);
+    const int64_t col = c0 + 4 * cq + j;
+    const int64_t rbase = r0 + rb * 16;
+    if (full) {
+      *reinterpret_cast<uint4 *>(p.q_col + col * p.ld_col + rbase) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else if (col < p.cols) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (rbase + e < p.rows) p.q_col[col * p.ld_col + rbase + e] = uint8_t(byte_of(w[e >> 2], e & 3));
+    }
+  }
+}
+
+template <bool BF16>
+hipError_t launch_fmt(const QuantParams &p, hipStream_t s, int64_t tiles, int64_t tiles_c, int aligned) {
+  if (p.fmt == 0)
+    hipLaunchKernelGGL((quantize_kernel<BF16, 0>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, p, tiles_c, aligned);
+  else
+    hipLaunchKernelGGL((quantize_kernel<BF16, 1>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, p, tiles_c, aligned);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const QuantParams &p, hipStream_t s) {
+  const int64_t tiles_r = (p.rows + kTile - 1) / kTile;
+  const int64_t tiles_c = (p.cols + kTile - 1) / kTile;
+  int64_t tiles = tiles_r * tiles_c;
+  if (tiles < 1) tiles = 1;  // still writes the scale_inv snapshot
+  const int64_t esize = p.in_bf16 ? 2 : 4;
+  const bool in_al = (reinterpret_cast<uintptr_t>(p.in) % 16 == 0) && ((p.cols * esize) % 16 == 0);
+  const bool row_al = p.q_row == nullptr || ((reinterpret_cast<uintptr_t>(p.q_row) % 16 == 0) && p.ld_row % 16 == 0);
+  const bool col_al = p.q_col == nullptr || ((reinterpret_cast<uintptr_t>(p.q_col) % 16 == 0) && p.ld_col % 16 == 0);
+  const int aligned = (in_al && row_al && col_al) ? 1 : 0;
+  const int64_t tc = tiles_c < 1 ? 1 : tiles_c;
+  return p.in_bf16 ? launch_fmt<true>(p, s, tiles, tc, aligned) : launch_fmt<false>(p, s, tiles, tc, aligned);
+}
+
+}  // namespace qe

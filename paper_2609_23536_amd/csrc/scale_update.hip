@@ -1,0 +1,93 @@
+// Delayed scale update from a rolling amax history (gfx950).
+//
+// The paper's delayed scaling (§2.1) derives each tensor role's scale from a
+// moving window of past amaxes; §3.2 fixes that F updates the forward roles
+// once and dI the gradient role once, and dW never.  Reading of the formula:
+//   a = max(history)  (NaN propagates)
+//   if a is finite and > 0:  e = floor(log2(fmax / a)) - margin, clamped to
+//                            [-126, 126]; scale = 2^e; scale_inv = 2^-e
+//   history rotates one place towards index 0 (index 0 -> H-1); index 0 = 0.
+// floor(log2(fmax/a)) is evaluated exactly on the bit pattern of a: with
+// a = m * 2^E, m in [1,2), and fmax = 1.75 * 2^Emax, it is Emax - E, minus one
+// when m > 1.75.  A float log2 would round 7 - tiny up to 7.
+//
+// One workgroup per role; the history is staged in LDS so the rotation is a
+// plain read-all / barrier / write-all.  Latency-bound (a few KB).
+#include "kernels.h"
+
+namespace qe {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    uint32_t o = __shfl_xor(v, off, 64);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(kThreads) void scale_update_kernel(UpdateParams p) {
+  extern __shared__ uint32_t hist_sh[];
+  __shared__ uint32_t red[kThreads / 64];
+  const MetaRef m = p.m[blockIdx.x];
+  const int H = m.history_len;
+  const int tid = threadIdx.x;
+
+  // amax values are >= +0 or a positive-signed NaN, so their bit patterns order
+  // like the values, and every NaN pattern sorts above +inf.
+  uint32_t mx = 0;
+  for (int i = tid; i < H; i += kThreads) {
+    uint32_t b = __float_as_uint(m.hist[i]) & 0x7fffffffu;
+    hist_sh[i] = b;
+    mx = b > mx ? b : mx;
+  }
+  mx = wave_max_u32(mx);
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+
+  if (tid == 0) {
+    uint32_t a = red[0];
+    for (int w = 1; w < kThreads / 64; ++w) a = red[w] > a ? red[w] : a;
+    if (a != 0u && a < 0x7f800000u) {
+      int E;
+      bool above;  // mantissa m > 1.75
+      if (a >= 0x00800000u) {
+        E = int(a >> 23) - 127;
+        above = (a & 0x007fffffu) > 0x00600000u;
+      } else {  // subnormal: a = f * 2^-149
+        int pbit = 31 - __clz(a);
+        E = pbit - 149;
+        above = (uint64_t(a) << 2) > (uint64_t(7) << pbit);
+      }
+      const int emax = m.fmt == 0 ? 8 : 15;
+      int e = emax - E - (above ? 1 : 0) - m.margin;
+      e = e < -126 ? -126 : (e > 126 ? 126 : e);
+      *m.scale = __uint_as_float(uint32_t(e + 127) << 23);
+      *m.scale_inv = __uint_as_float(uint32_t(127 - e) << 23);
+    }
+    if (blockIdx.x == 0 && p.token != nullptr) *p.token += 1;
+  }
+  // Rotate: new[i] = old[i+1] (i < H-1), new[H-1] = old[0], then new[0] = 0.
+  for (int i = tid; i < H; i += kThreads) {
+    float v;
+    if (i == 0)
+      v = 0.0f;
+    else
+      v = __uint_as_float(i == H - 1 ? hist_sh[0] : hist_sh[i + 1]);
+    m.hist[i] = v;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s) {
+  int hmax = 0;
+  for (int i = 0; i < p.n; ++i) hmax = p.m[i].history_len > hmax ? p.m[i].history_len : hmax;
+  size_t lds = size_t(hmax) * sizeof(uint32_t);
+  hipLaunchKernelGGL(scale_update_kernel, dim3(p.n), dim3(kThreads), lds, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace qe

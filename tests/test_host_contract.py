@@ -1,0 +1,233 @@
+"""The library's contract (null executor: no HIP call, no device) against the
+oracle's state machine, call by call and state by state."""
+import random
+
+import pytest
+
+from oracle import contract as OC
+from tests.libqe import need_lib
+
+BUF = 1 << 20          # fake buffer base address (never dereferenced in null mode)
+BUF_ELEMS = 1 << 22
+
+
+class Pair:
+    """Runs every call on both the oracle contract and the library, compares status and state."""
+
+    def __init__(self, M, layers):
+        qe = need_lib()
+        self.qe = qe
+        self.o = OC.Contract(M)
+        self.c = qe.Context(M, null_executor=True)
+        self.M = M
+        self.refs_o, self.refs_c = {}, {}
+        for u, (n, k, t) in enumerate(layers):
+            self.o.add_layer(0, u, n, k, t)
+            st, idx = self.c.qe_layer_register(0, u, n, k, t, 0, qe.F32, 4, 0)
+            assert st == "OK" and idx == u
+
+    def state(self):
+        ctx = self.c.qe_get_state()
+        snap = {"e_w": ctx["e_w"], "token": ctx["token"], "arena_valid": bool(ctx["arena_valid"]),
+                "finalized": bool(ctx["finalized"]), "layers": [], "written": {}}
+        for l in range(len(self.o.layers)):
+            ls = self.c.qe_get_layer_state(l)
+            slots = []
+            for m in range(self.M):
+                s = self.c.qe_get_slot_state(l, m)
+                slots.append((s["live"], s["key"] if s["live"] else None, s["generation"], s["bits"],
+                              s["tokens"] if s["live"] else 0))
+                if s["bound"]:
+                    snap["written"][(l, m)] = s["written"]
+            snap["layers"].append({"e_c": ls["e_c"], "refreshes": ls["refreshes"], "slots": slots})
+        return snap
+
+    def check(self):
+        assert self.state() == self.o.snapshot()
+
+    def fwd(self, l, k, tokens=8):
+        st, refresh = self.o.check_fwd(l, k, tokens)
+        if st == OC.OK:
+            if self.o._physical_fails():
+                self.o.abort()
+                st = OC.EXEC_FAILED
+            else:
+                self.o.commit_fwd(l, k, tokens, refresh)
+        st_c, ref = self.c.qe_fp8_linear_fwd(l, self.qe.key(*k), 0, self.qe.F32, tokens, 0, self.qe.F32)
+        assert st_c == st, ("fwd", l, k, st_c, st)
+        return st, ref
+
+    def dgrad(self, l, k, ref):
+        st = self.o.check_dgrad(l, k, ref)
+        if st == OC.OK:
+            if self.o._physical_fails():
+                self.o.abort()
+                st = OC.EXEC_FAILED
+            else:
+                self.o.commit_dgrad(l, ref)
+        st_c = self.c.qe_fp8_linear_dgrad(l, self.qe.key(*k), ref, 0, self.qe.F32, 0, self.qe.F32)
+        assert st_c == st, ("dI", l, k, ref, st_c, st)
+        return st
+
+    def wgrad(self, l, k, ref, off, ld, mode, buf=BUF):
+        st = self.o.check_wgrad(l, k, ref, buf, off, ld, mode)
+        if st == OC.OK:
+            if self.o._physical_fails():
+                self.o.abort()
+                st = OC.EXEC_FAILED
+            else:
+                self.o.commit_wgrad(l, ref)
+        st_c = self.c.qe_fp8_linear_wgrad_place(l, self.qe.key(*k), ref, buf, off, ld, mode)
+        assert st_c == st, ("dW", l, k, ref, st_c, st)
+        return st
+
+    def full(self, l, k, ref, off, ld, mode, buf=BUF):
+        st = self.o.check_bwd_full(l, k, ref, buf, off, ld, mode)
+        if st == OC.OK:
+            if self.o._physical_fails():
+                self.o.abort()
+                st = OC.EXEC_FAILED
+            else:
+                self.o.commit_bwd_full(l, ref)
+        st_c = self.c.qe_fp8_linear_bwd_full(l, self.qe.key(*k), ref, 0, self.qe.F32, 0, self.qe.F32, buf, off,
+                                             ld, mode)
+        assert st_c == st, ("full", l, k, ref, st_c, st)
+        return st
+
+    def bind(self, l, m, off, ld, buf=BUF, elems=BUF_ELEMS):
+        st = self.o.bind(l, m, buf, elems, off, ld)
+        assert self.c.qe_arena_bind(l, m, buf, elems, off, ld) == st
+        return st
+
+    def finalize(self):
+        st = self.o.finalize()
+        assert self.c.qe_arena_finalize() == st
+        return st
+
+    def commit(self):
+        st = self.o.optimizer_commit()
+        assert self.c.qe_optimizer_commit() == st
+        return st
+
+    def abort(self):
+        self.o.abort()
+        assert self.c.qe_abort_epoch() == "OK"
+
+    def rebuild(self):
+        assert self.c.qe_arena_rebuild() == self.o.rebuild()
+
+    def inject(self, n):
+        self.o.inject_fault(n)
+        assert self.c.qe_inject_fault(n) == "OK"
+
+
+def K(e, m, u=0, inv=0):
+    return (e, 0, m, u, inv)
+
+
+def test_fault_table_rows():
+    p = Pair(2, [(4, 8, 16)])
+    p.bind(0, 0, 0, 8)
+    p.bind(0, 1, 64, 8)
+    # old reference after slot reuse
+    _, r0 = p.fwd(0, K(0, 0))
+    p.dgrad(0, K(0, 0), r0)
+    p.wgrad(0, K(0, 0), r0, 0, 8, OC.INIT)
+    _, r0b = p.fwd(0, K(0, 0, inv=1))
+    assert p.dgrad(0, K(0, 0), r0) == OC.STALE_REF
+    p.check()
+    # repeated dI
+    assert p.dgrad(0, K(0, 0, inv=1), r0b) == OC.OK
+    assert p.dgrad(0, K(0, 0, inv=1), r0b) == OC.DUPLICATE_CONSUMER
+    assert p.wgrad(0, K(0, 0, inv=1), r0b, 0, 8, OC.INIT) == OC.DUP_WRITE   # view 0 already written
+    p.check()
+    # finalize with a missing dW
+    _, r1 = p.fwd(0, K(0, 1))
+    p.dgrad(0, K(0, 1), r1)
+    assert p.finalize() == OC.INCOMPLETE
+    assert p.commit() == OC.NOT_QUIESCENT
+    p.check()
+    # write after an aborted write
+    p.inject(1)
+    assert p.wgrad(0, K(0, 1), r1, 64, 8, OC.INIT) == OC.EXEC_FAILED
+    assert p.wgrad(0, K(0, 1), r1, 64, 8, OC.INIT) == OC.ARENA_INVALID
+    assert p.finalize() == OC.ARENA_INVALID
+    p.check()
+    p.rebuild()
+    p.check()
+    # stale cache: after a commit, a microbatch-1 forward before microbatch 0
+    _, r0 = p.fwd(0, K(0, 0, inv=2))
+    p.full(0, K(0, 0, inv=2), r0, 0, 8, OC.INIT)
+    _, r1 = p.fwd(0, K(0, 1, inv=2))
+    p.full(0, K(0, 1, inv=2), r1, 64, 8, OC.INIT)
+    assert p.finalize() == OC.OK and p.commit() == OC.OK
+    assert p.fwd(0, K(1, 1))[0] == OC.STALE_CACHE
+    assert p.fwd(0, K(1, 0))[0] == OC.OK
+    p.check()
+
+
+def test_bind_rules():
+    p = Pair(2, [(4, 8, 16), (3, 5, 16)])
+    assert p.bind(0, 0, 0, 8) == OC.OK
+    assert p.bind(0, 1, 0, 8) == OC.OK
+    assert p.bind(1, 0, 20, 5) == OC.DEST_ALIAS
+    assert p.bind(1, 0, 32, 5) == OC.OK
+    assert p.bind(1, 1, 33, 5) == OC.DEST_ALIAS
+    assert p.bind(1, 1, 0, 4) == OC.INVALID_ARG
+    assert p.bind(1, 1, BUF_ELEMS - 5, 5) == OC.INVALID_ARG
+    assert p.bind(1, 1, 100, 5, buf=0) == OC.INVALID_ARG
+    assert p.bind(2, 0, 100, 5) == OC.INVALID_ARG
+    p.check()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_schedules_match_oracle(seed):
+    rng = random.Random(seed)
+    M, nl = rng.choice([1, 2, 3, 4]), rng.choice([1, 2])
+    p = Pair(M, [(4, 8, 16)] * nl)
+    for u in range(nl):
+        for m in range(M):
+            shared = rng.random() < 0.3
+            p.bind(u, m, (u * M + (0 if shared else m)) * 64, 8)
+    refs = {}
+    for _ in range(300):
+        u, m = rng.randrange(nl), rng.randrange(M)
+        e = p.o.e_w + (0 if rng.random() < 0.9 else rng.choice([-1, 1]))
+        k = K(max(e, 0), m, u, rng.choice([0, 0, 0, 1]))
+        ref = refs.get((u, m), (m, 0))
+        if rng.random() < 0.1:
+            ref = (ref[0], ref[1] + rng.choice([-1, 1, 2]))
+        if rng.random() < 0.03:
+            p.inject(rng.randint(1, 3))
+        b = p.o.bindings.get((u, m))
+        off = b.offset if b else 0
+        mode = OC.ACCUM if (b and any(o.written and o.start() == b.start() for o in p.o.bindings.values())) \
+            else OC.INIT
+        if rng.random() < 0.05:
+            mode = 1 - mode
+        what = rng.choice(["f", "f", "di", "dw", "full", "fin", "commit", "abort", "rebuild"])
+        if what == "f":
+            st, r = p.fwd(u, k, tokens=rng.randint(0, 16))
+            if st == OC.OK:
+                refs[(u, m)] = r
+                # keep the key of this tape for its consumers
+                refs[("key", u, m)] = k
+        elif what in ("di", "dw", "full"):
+            kk = refs.get(("key", u, m), k)
+            if rng.random() < 0.1:
+                kk = k
+            if what == "di":
+                p.dgrad(u, kk, ref)
+            elif what == "dw":
+                p.wgrad(u, kk, ref, off, 8, mode)
+            else:
+                p.full(u, kk, ref, off, 8, mode)
+        elif what == "fin":
+            p.finalize()
+        elif what == "commit":
+            p.commit()
+        elif what == "abort" and rng.random() < 0.2:
+            p.abort()
+        elif what == "rebuild":
+            p.rebuild()
+        p.check()
