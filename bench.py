@@ -1,0 +1,219 @@
+"""Benchmark: one pass of the FP8 split-linear hot path over a Llama-shaped stage.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--eager]
+
+A step runs, for every linear of the stage (QKV, O, gate+up, down of the
+Llama-3-8B shape by default, 4096 tokens, bf16 inputs and master weights,
+amax history 1024):  F (with the weight-cache refresh, since every step
+follows a version bump), then dI and the deferred dW with direct placement
+into one flat FP32 main-gradient buffer, then arena finalize and optimizer
+commit.  Every action is one HIP-graph replay behind the two-way handoff.
+Inputs are synthetic, seeded, and resident in HBM before timing starts.
+
+Prints one JSON line.  `value` is GEMM FLOPs (fwd + dI + dW, 2*M*N*K each)
+per second over the whole step, quantization and scale updates included.
+`roofline` is the GEMM kernel alone, timed with HIP events on the stream the
+library launches it on, in an instrumented eager pass over the same steps.
+`cpu_baseline` times the CPU oracle on a bounded sample (one linear, a few
+hundred tokens).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP8_PEAK_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
+METRIC = "FP8 fwd+dI+dW TFLOP/s (% FP8 MFMA peak); quantize/wgrad-place GB/s (% HBM)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3_8b_stage_4096tok")
+    ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of graph replay")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    return ap.parse_args()
+
+
+class StageBench:
+    def __init__(self, qe, torch, wl, use_graphs, device):
+        import workloads as W
+        self.qe, self.torch, self.wl, self.d = qe, torch, wl, device
+        self.ctx = qe.Context(1, use_graphs=use_graphs)
+        self.n_lin = len(wl.linears)
+        bf = wl.in_dtype == "bf16"
+        self.dt = qe.BF16 if bf else qe.F32
+        tdt = torch.int16 if bf else torch.float32
+
+        def up(t):
+            import numpy as np
+            a = t.data.view(np.int16) if bf else t.data
+            return torch.from_numpy(a).to(device)
+
+        self.w, self.x, self.dy, self.y, self.dx = [], [], [], [], []
+        for u, lin in enumerate(wl.linears):
+            self.w.append(up(W.layer_weight(wl, u)))
+            inp = W.layer_inputs(wl, u)
+            self.x.append(up(inp["x"]))
+            self.dy.append(up(inp["dy"]))
+            self.y.append(torch.empty((wl.tokens, lin.n_out), dtype=tdt, device=device))
+            self.dx.append(torch.empty((wl.tokens, lin.k_in), dtype=tdt, device=device))
+            st, idx = self.ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, wl.tokens, self.w[u], self.dt,
+                                                 wl.history, wl.margin)
+            assert st == "OK" and idx == u, st
+        self.grad = torch.zeros(wl.flat_grad_elems(), dtype=torch.float32, device=device)
+        self.offs = wl.grad_offsets()
+        for u, lin in enumerate(wl.linears):
+            st = self.ctx.qe_arena_bind(u, 0, self.grad, self.grad.numel(), self.offs[u], lin.k_in)
+            assert st == "OK", st
+        self.epoch = 0
+
+    def step(self):
+        qe, wl, ctx = self.qe, self.wl, self.ctx
+        refs = []
+        for u in range(self.n_lin):
+            st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(self.epoch, 0, 0, u), self.x[u], self.dt, wl.tokens,
+                                            self.y[u], self.dt)
+            assert st == "OK", st
+            refs.append(ref)
+        for u in reversed(range(self.n_lin)):
+            k = qe.key(self.epoch, 0, 0, u)
+            st = ctx.qe_fp8_linear_dgrad(u, k, refs[u], self.dy[u], self.dt, self.dx[u], self.dt)
+            assert st == "OK", st
+            st = ctx.qe_fp8_linear_wgrad_place(u, k, refs[u], self.grad, self.offs[u], wl.linears[u].k_in, qe.INIT)
+            assert st == "OK", st
+        assert ctx.qe_arena_finalize() == "OK"
+        assert ctx.qe_optimizer_commit() == "OK"
+        self.epoch += 1
+
+
+def algorithmic_bytes(wl):
+    """Per step: quantize bytes (in + row codes + column codes) of X, dY and the W refresh."""
+    b_in = 2 if wl.in_dtype == "bf16" else 4
+    q = 0
+    for lin in wl.linears:
+        q += wl.tokens * lin.k_in * (b_in + 2)       # X
+        q += wl.tokens * lin.n_out * (b_in + 2)      # dY
+        q += lin.n_out * lin.k_in * (b_in + 2)       # W refresh
+    return q
+
+
+def cpu_baseline(wl, tokens):
+    """The oracle as it stands on one linear (the first) with `tokens` rows: F, dI, dW."""
+    import numpy as np
+    import workloads as W
+    from oracle import contract as OC
+    from oracle.layer import Stage
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    lin = wl.linears[0]
+    inp = W.layer_inputs(wl, 0, tokens=tokens)
+    w = W.layer_weight(wl, 0).as_f32()
+    t0 = time.perf_counter()
+    st = Stage(1)
+    st.add_layer(0, 0, w, tokens, wl.history, wl.margin)
+    st.add_buffer(4096, lin.n_out * lin.k_in)
+    st.bind(0, 0, 4096, 0, lin.k_in)
+    key = (0, 0, 0, 0, 0)
+    s, y, ref = st.fwd(0, key, inp["x"].as_f32())
+    s2, dx = st.dgrad(0, key, ref, inp["dy"].as_f32())
+    s3 = st.wgrad_place(0, key, ref, 4096, 0, lin.k_in, OC.INIT)
+    el = time.perf_counter() - t0
+    assert s == s2 == s3 == OC.OK
+    flops = 3 * 2 * tokens * lin.n_out * lin.k_in
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{lin.name} {lin.k_in}->{lin.n_out}, {tokens} tokens: F (with W quantize) + dI + dW "
+                      f"through the float64 oracle, {el:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    import workloads as W
+    from paper_2609_23536_amd import qe
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+    qe.lib()
+    dev = torch.device("cuda:0")
+    wl = W.WORKLOADS[args.workload]
+    use_graphs = not args.eager
+
+    b = StageBench(qe, torch, wl, use_graphs, dev)
+    for _ in range(args.warmup):
+        b.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        b.step()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    assert b.ctx.qe_sync() == "OK"
+    st = b.ctx.qe_get_state()
+    assert st["device_token"] == st["token"]
+
+    flops = wl.gemm_flops_per_pass()
+    ms = el / args.steps * 1e3
+    value = flops / (el / args.steps) / 1e12
+
+    # instrumented eager pass: per-kernel-class times from HIP events on the graph stream
+    b.ctx.close()
+    del b
+    torch.cuda.empty_cache()
+    e = StageBench(qe, torch, wl, False, dev)
+    e.step()
+    torch.cuda.synchronize()
+    e.ctx.qe_set_kernel_timing(True)
+    for _ in range(args.steps):
+        e.step()
+    gemm_ms, gemm_n = e.ctx.qe_get_kernel_timing(qe.KC_GEMM)
+    q_ms, q_n = e.ctx.qe_get_kernel_timing(qe.KC_QUANT)
+    u_ms, u_n = e.ctx.qe_get_kernel_timing(qe.KC_UPDATE)
+    e.ctx.close()
+    gemm_tflops = flops * args.steps / (gemm_ms * 1e-3) / 1e12
+    qbytes = algorithmic_bytes(wl)
+    q_gbs = qbytes * args.steps / (q_ms * 1e-3) / 1e9
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8(e4m3 x,w / e5m2 dy), f32 accumulate", "data": "synthetic",
+        "config": {"workload": wl.key, "tokens": wl.tokens, "microbatches": wl.microbatches,
+                   "linears": [[l.name, l.k_in, l.n_out] for l in wl.linears], "in_dtype": wl.in_dtype,
+                   "amax_history": wl.history, "graphs": use_graphs},
+        "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_tn_kernel (fwd + dI + dW launches)",
+                     "avg_launch_us": round(gemm_ms / gemm_n * 1e3, 2), "launches": gemm_n},
+        "quantize": {"achieved": round(q_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                     "frac": round(q_gbs / HBM_PEAK_GBS, 4), "avg_launch_us": round(q_ms / q_n * 1e3, 2),
+                     "launches": q_n},
+        "scale_update": {"avg_launch_us": round(u_ms / u_n * 1e3, 2), "launches": u_n},
+        "graph": {"captures": st["captures"], "replays": st["replays"], "handoffs": st["handoffs"],
+                  "capture_ms": round(st["capture_ns"] / 1e6, 2)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

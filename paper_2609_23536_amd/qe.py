@@ -113,6 +113,12 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_23536_amd.build`")
+        # torch ships its own HIP runtime under the same soname; load it first so
+        # that the library and torch's allocator and streams share one runtime.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = C.CDLL(LIB_PATH)
         for name, args in _SIGS.items():
             fn = getattr(L, name)

@@ -1,0 +1,199 @@
+"""Runs an action schedule on the library (GPU) and on the oracle with the same
+seeded inputs, so tests can compare them action by action."""
+import numpy as np
+
+import workloads as W
+from oracle import contract as OC
+from oracle.layer import Stage
+from tests.gpu_util import dev_bytes, dev_f32, torch, upload
+
+
+class Spec:
+    def __init__(self, shapes, tokens, M, history, margin, in_dtype, shared_view, out_dtype="f32", seed=0,
+                 cfg=90, outliers=False):
+        self.shapes, self.tokens, self.M = shapes, tokens, M
+        self.history, self.margin, self.in_dtype = history, margin, in_dtype
+        self.shared_view, self.out_dtype, self.seed, self.cfg = shared_view, out_dtype, seed, cfg
+        self.outliers = outliers
+
+    def total(self):
+        return sum(n * k for n, k in self.shapes)
+
+    def offset(self, u, m):
+        offs = np.cumsum([0] + [n * k for n, k in self.shapes])
+        return int(offs[u] if self.shared_view else m * self.total() + offs[u])
+
+    def grad_elems(self):
+        return self.total() * (1 if self.shared_view else self.M)
+
+    def weight(self, u):
+        n, k = self.shapes[u]
+        return W.normal(W.rng_for(self.seed, self.cfg, u, W.ROLE_W), (n, k), 0.02, self.in_dtype)
+
+    def inputs(self, u, m, step):
+        n, k = self.shapes[u]
+        rx = W.rng_for(self.seed, self.cfg, u, W.ROLE_X, m, step)
+        rd = W.rng_for(self.seed, self.cfg, u, W.ROLE_DY, m, step)
+        if self.outliers:
+            x = W.outlier_activations(rx, self.tokens, k, 0.001 if k >= 1000 else 0.02, 300.0, self.in_dtype)
+            dy = W.lognormal_signed(rd, (self.tokens, n), 2.0, self.in_dtype)
+        else:
+            x = W.normal(rx, (self.tokens, k), 1.0, self.in_dtype)
+            dy = W.normal(rd, (self.tokens, n), 0.01, self.in_dtype)
+        return x, dy
+
+
+class GpuStage:
+    def __init__(self, qe, spec, use_graphs=False, device=None):
+        self.qe, self.spec = qe, spec
+        self.d = device
+        self.ctx = qe.Context(spec.M, use_graphs=use_graphs)
+        dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
+        self.w = [upload(spec.weight(u), self.d) for u in range(len(spec.shapes))]
+        for u, (n, k) in enumerate(spec.shapes):
+            st, idx = self.ctx.qe_layer_register(0, u, n, k, spec.tokens, self.w[u], dt, spec.history, spec.margin)
+            assert st == "OK" and idx == u
+        self.grad = torch.zeros(spec.grad_elems(), dtype=torch.float32, device=self.d)
+        for u, (n, k) in enumerate(spec.shapes):
+            for m in range(spec.M):
+                assert self.ctx.qe_arena_bind(u, m, self.grad, spec.grad_elems(), spec.offset(u, m), k) == "OK"
+        self.refs = {}
+        self.written = set()
+        self.outs = {}
+
+    def _out(self, rows, cols):
+        if self.spec.out_dtype == "bf16":
+            return torch.zeros((rows, cols), dtype=torch.int16, device=self.d)
+        return torch.zeros((rows, cols), dtype=torch.float32, device=self.d)
+
+    def _mode(self, u, m):
+        off = self.spec.offset(u, m)
+        return self.qe.ACCUM if (u, off) in self.written else self.qe.INIT
+
+    def run(self, schedule, epoch, step):
+        qe, spec = self.qe, self.spec
+        dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
+        odt = qe.BF16 if spec.out_dtype == "bf16" else qe.F32
+        for a, m in schedule:
+            for u, (n, k) in enumerate(spec.shapes):
+                key = qe.key(epoch, 0, m, u)
+                x, dy = spec.inputs(u, m, step)
+                if a == "F":
+                    y = self._out(spec.tokens, n)
+                    st, self.refs[(u, m)] = self.ctx.qe_fp8_linear_fwd(u, key, upload(x, self.d), dt, spec.tokens,
+                                                                       y, odt)
+                    self.outs[("y", u, m, step)] = y
+                elif a == "dI":
+                    dx = self._out(spec.tokens, k)
+                    st = self.ctx.qe_fp8_linear_dgrad(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt)
+                    self.outs[("dx", u, m, step)] = dx
+                elif a == "dW":
+                    mode = self._mode(u, m)
+                    st = self.ctx.qe_fp8_linear_wgrad_place(u, key, self.refs[(u, m)], self.grad, spec.offset(u, m),
+                                                            k, mode)
+                    self.written.add((u, spec.offset(u, m)))
+                else:
+                    dx = self._out(spec.tokens, k)
+                    mode = self._mode(u, m)
+                    st = self.ctx.qe_fp8_linear_bwd_full(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt,
+                                                         self.grad, spec.offset(u, m), k, mode)
+                    self.written.add((u, spec.offset(u, m)))
+                    self.outs[("dx", u, m, step)] = dx
+                assert st == "OK", (a, m, u, st)
+
+    def end_step(self, new_weights=None):
+        assert self.ctx.qe_arena_finalize() == "OK"
+        if new_weights is not None:
+            torch.cuda.synchronize()
+            for u, w in enumerate(new_weights):
+                self.w[u].copy_(upload(w, self.d))
+        assert self.ctx.qe_optimizer_commit() == "OK"
+        self.written = set()
+
+    def fp8_state(self, u):
+        H = self.spec.history
+        out = {}
+        for name, role in (("x", self.qe.ROLE_X), ("w", self.qe.ROLE_W), ("dy", self.qe.ROLE_DY)):
+            m = self.ctx.qe_layer_meta(u, role)
+            h = dev_f32(m.amax_history, H, self.d)
+            s = dev_f32(m.scale, 1, self.d)[0]
+            si = dev_f32(m.scale_inv, 1, self.d)[0]
+            out[name] = (h, s, si)
+        return out
+
+    def slot_codes(self, u, m):
+        n, k = self.spec.shapes[u]
+        p = self.ctx.qe_layer_slot_payload(u, m)
+        t = self.spec.tokens
+        xt = dev_bytes(p["x_q_t"], k * p["ld_x_q_t"], self.d).reshape(k, p["ld_x_q_t"])[:, :t]
+        dyt = dev_bytes(p["dy_q_t"], n * p["ld_dy_q_t"], self.d).reshape(n, p["ld_dy_q_t"])[:, :t]
+        return xt, dyt
+
+    def cache_codes(self, u):
+        n, k = self.spec.shapes[u]
+        c = self.ctx.qe_layer_cache(u)
+        wq = dev_bytes(c["w_q"], n * c["ld_w_q"], self.d).reshape(n, c["ld_w_q"])[:, :k]
+        wqt = dev_bytes(c["w_q_t"], k * c["ld_w_q_t"], self.d).reshape(k, c["ld_w_q_t"])[:, :n]
+        return wq, wqt
+
+
+class OracleStage:
+    def __init__(self, spec):
+        self.spec = spec
+        self.st = Stage(spec.M)
+        for u, (n, k) in enumerate(spec.shapes):
+            self.st.add_layer(0, u, spec.weight(u).as_f32(), spec.tokens, spec.history, spec.margin)
+        self.buf = 1 << 12
+        self.st.add_buffer(self.buf, spec.grad_elems())
+        for u, (n, k) in enumerate(spec.shapes):
+            for m in range(spec.M):
+                assert self.st.bind(u, m, self.buf, spec.offset(u, m), k) == OC.OK
+        self.refs = {}
+        self.outs = {}
+
+    def _mode(self, u, m):
+        b = self.st.contract.bindings[(u, m)]
+        init = not any(o.written and o.start() == b.start() for o in self.st.contract.bindings.values())
+        return OC.INIT if init else OC.ACCUM
+
+    def run(self, schedule, epoch, step):
+        spec = self.spec
+        for a, m in schedule:
+            for u, (n, k) in enumerate(spec.shapes):
+                key = (epoch, 0, m, u, 0)
+                x, dy = spec.inputs(u, m, step)
+                if a == "F":
+                    st, y, self.refs[(u, m)] = self.st.fwd(u, key, x.as_f32())
+                    self.outs[("y", u, m, step)] = y
+                elif a == "dI":
+                    st, self.outs[("dx", u, m, step)] = self.st.dgrad(u, key, self.refs[(u, m)], dy.as_f32())
+                elif a == "dW":
+                    st = self.st.wgrad_place(u, key, self.refs[(u, m)], self.buf, spec.offset(u, m), k,
+                                             self._mode(u, m))
+                else:
+                    st, self.outs[("dx", u, m, step)] = self.st.bwd_full(u, key, self.refs[(u, m)], dy.as_f32(),
+                                                                         self.buf, spec.offset(u, m), k,
+                                                                         self._mode(u, m))
+                assert st == OC.OK, (a, m, u, st)
+
+    def sgd_weights(self, lr=1e-3):
+        """W <- W - lr * sum of the step's gradient views, rounded like the inputs."""
+        spec = self.spec
+        g = self.st.arena[self.buf]
+        new = []
+        for u, (n, k) in enumerate(spec.shapes):
+            acc = np.zeros((n, k), dtype=np.float64)
+            for m in range(1 if spec.shared_view else spec.M):
+                o = spec.offset(u, m)
+                acc += g[o:o + n * k].reshape(n, k)
+            w = (self.st.layers[u].w.astype(np.float64) - lr * acc).astype(np.float32)
+            t = W.Tensor(W.f32_to_bf16_bits(w), "bf16") if spec.in_dtype == "bf16" else W.Tensor(w, "f32")
+            new.append(t)
+        return new
+
+    def end_step(self, new_weights=None):
+        assert self.st.finalize() == OC.OK
+        if new_weights is not None:
+            for u, w in enumerate(new_weights):
+                self.st.set_weight(u, w.as_f32())
+        assert self.st.optimizer_commit() == OC.OK

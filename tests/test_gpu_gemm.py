@@ -1,0 +1,141 @@
+"""FP8 GEMM parity on the GPU against the oracle's float64 product.
+
+Bar: max |G - O| / max |O| <= 1e-3 per output (FP32 accumulation against an
+exact-product float64 sum); bit-exact where every partial sum is an integer
+below 2^24 (then FP32 accumulation is exact in any order)."""
+import numpy as np
+import pytest
+
+from oracle import fp8, gemm
+from tests.gpu_util import dev, rel_err, torch
+from tests.libqe import need_lib
+
+pytestmark = pytest.mark.gpu
+FMTS = {0: "E4M3", 1: "E5M2"}
+
+
+def rup16(v):
+    return (v + 15) // 16 * 16
+
+
+def random_codes(rng, rows, cols, fmt, ld):
+    c = rng.integers(0, 256, size=(rows, ld), dtype=np.uint8)
+    if fmt == 0:
+        c[(c & 0x7F) == 0x7F] = 0x3C          # no NaN
+    else:
+        c[(c & 0x7C) == 0x7C] = 0x3C          # no inf / NaN
+        c &= 0xBF                             # keep |values| <= 2^0 range-ish (exponent field < 16)
+    return c
+
+
+def run_gemm(qe, d, A, fa, B, fb, m, n, k, sa, sb, out, ldc, mode=0, c_init=None):
+    lda, ldb = A.shape[1], B.shape[1]
+    a_t = torch.from_numpy(A).to(d)
+    b_t = torch.from_numpy(B).to(d)
+    s = torch.tensor([sa, sb], dtype=torch.float32, device=d)
+    if out == qe.BF16:
+        c_t = torch.zeros(max(m * ldc, 1), dtype=torch.int16, device=d)
+    else:
+        c_t = torch.from_numpy(c_init.copy()).to(d) if c_init is not None else \
+            torch.zeros(max(m * ldc, 1), dtype=torch.float32, device=d)
+    st = qe.qe_fp8_gemm_tn(a_t, fa, lda, b_t, fb, ldb, m, n, k, s[0:1], s[1:2], c_t, out, ldc, mode)
+    assert st == "OK", st
+    torch.cuda.synchronize()
+    c = c_t.cpu().numpy()
+    if out == qe.BF16:
+        c = (c.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    return c
+
+
+SHAPES = [(1, 1, 1), (16, 16, 128), (37, 53, 100), (256, 256, 128), (300, 520, 384), (513, 257, 1000),
+          (128, 256, 256), (64, 96, 16), (255, 511, 129)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("fa,fb", [(0, 0), (1, 0), (0, 1), (1, 1)])
+def test_random_codes(shape, fa, fb):
+    qe = need_lib()
+    d = dev()
+    m, n, k = shape
+    rng = np.random.default_rng(m * 7 + n * 13 + k + fa * 2 + fb)
+    A = random_codes(rng, m, k, fa, rup16(k))
+    B = random_codes(rng, n, k, fb, rup16(k))
+    sa, sb = 2.0 ** -3, 2.0 ** 5
+    ref = gemm.gemm_tn(A[:, :k], FMTS[fa], B[:, :k], FMTS[fb], sa, sb)
+    got = run_gemm(qe, d, A, fa, B, fb, m, n, k, sa, sb, qe.F32, n)[: m * n].reshape(m, n)
+    assert rel_err(got, ref) <= 1e-3
+
+
+@pytest.mark.parametrize("shape", [(37, 53, 100), (300, 520, 384), (256, 512, 4096)], ids=str)
+def test_integer_operands_bit_exact(shape):
+    """Codes of small integers: every partial sum is an integer < 2^24, so the
+    FP32 result must equal the exact integer product bit for bit."""
+    qe = need_lib()
+    d = dev()
+    m, n, k = shape
+    rng = np.random.default_rng(5)
+    ai = rng.integers(-6, 7, size=(m, k))
+    bi = rng.integers(-6, 7, size=(n, k))
+    A = np.zeros((m, rup16(k)), dtype=np.uint8)
+    B = np.zeros((n, rup16(k)), dtype=np.uint8)
+    A[:, :k] = fp8.encode(ai.astype(np.float64), "E4M3")
+    B[:, :k] = fp8.encode(bi.astype(np.float64), "E5M2")
+    got = run_gemm(qe, d, A, 0, B, 1, m, n, k, 1.0, 0.5, qe.F32, n)[: m * n].reshape(m, n)
+    np.testing.assert_array_equal(got, (ai @ bi.T).astype(np.float32) * np.float32(0.5))
+
+
+def test_bf16_output():
+    qe = need_lib()
+    d = dev()
+    m, n, k = 200, 300, 512
+    rng = np.random.default_rng(9)
+    A = random_codes(rng, m, k, 0, k)
+    B = random_codes(rng, n, k, 0, k)
+    ref = gemm.gemm_tn(A, "E4M3", B, "E4M3", 0.25, 0.125)
+    got = run_gemm(qe, d, A, 0, B, 0, m, n, k, 0.25, 0.125, qe.BF16, n)[: m * n].reshape(m, n)
+    # a bf16 result is within half a bf16 ulp (2^-9 relative, 2^-8 at worst
+    # across a binade edge) of the FP32 accumulation, which is within 1e-3
+    assert rel_err(got, ref) <= 2.0 ** -8 + 1e-3
+
+
+@pytest.mark.parametrize("shape", [(40, 70, 64), (256, 256, 256), (300, 257, 130)], ids=str)
+def test_accumulate_strided_view_untouched_elsewhere(shape):
+    """ACCUM into a strided view of a flat buffer: the view gets fl32(G + D);
+    every other element (before, after, and the row gaps) keeps its sentinel."""
+    qe = need_lib()
+    d = dev()
+    m, n, k = shape
+    ldc, off = n + 9, 37
+    rng = np.random.default_rng(3)
+    A = random_codes(rng, m, k, 1, rup16(k))
+    B = random_codes(rng, n, k, 0, rup16(k))
+    total = off + (m - 1) * ldc + n + 50
+    G = rng.standard_normal(total).astype(np.float32)
+    a_t, b_t = torch.from_numpy(A).to(d), torch.from_numpy(B).to(d)
+    s = torch.tensor([0.5, 2.0], dtype=torch.float32, device=d)
+    g_t = torch.from_numpy(G.copy()).to(d)
+    view = g_t[off:]
+    assert qe.qe_fp8_gemm_tn(a_t, 1, A.shape[1], b_t, 0, B.shape[1], m, n, k, s[0:1], s[1:2], view, qe.F32, ldc,
+                             qe.ACCUM) == "OK"
+    torch.cuda.synchronize()
+    got = g_t.cpu().numpy()
+    ref = G.copy()
+    gemm.place(ref, gemm.gemm_tn(A[:, :k], "E5M2", B[:, :k], "E4M3", 0.5, 2.0), off, ldc, accumulate=True)
+    idx = gemm.view_index(off, ldc, m, n)
+    mask = np.ones(total, dtype=bool)
+    mask[idx.ravel()] = False
+    np.testing.assert_array_equal(got[mask], G[mask])
+    assert rel_err(got[idx], ref[idx]) <= 1e-3
+
+
+def test_k_zero_and_empty():
+    qe = need_lib()
+    d = dev()
+    A = np.zeros((8, 16), dtype=np.uint8)
+    B = np.zeros((4, 16), dtype=np.uint8)
+    got = run_gemm(qe, d, A, 0, B, 0, 8, 4, 0, 1.0, 1.0, qe.F32, 4, c_init=np.full(32, 3.0, dtype=np.float32))
+    np.testing.assert_array_equal(got, np.zeros(32, dtype=np.float32))
+    got = run_gemm(qe, d, A, 0, B, 0, 8, 4, 0, 1.0, 1.0, qe.F32, 4, mode=1,
+                   c_init=np.full(32, 3.0, dtype=np.float32))
+    np.testing.assert_array_equal(got, np.full(32, 3.0, dtype=np.float32))
+    assert qe.qe_fp8_gemm_tn(0, 0, 16, 0, 0, 16, 0, 4, 16, 0, 0, 0, qe.F32, 4) == "OK"
