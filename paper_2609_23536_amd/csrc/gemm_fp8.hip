@@ -38,21 +38,20 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int BK = 128;
 constexpr int kGroupM = 8;
 
+constexpr int kCUs = 256;  // MI355X compute units; one 128 KB-LDS workgroup each
+
 __device__ __forceinline__ uint32_t lds_off(int row, int chunk) {
   return uint32_t(row) * BK + (uint32_t((chunk ^ (row >> 1)) & 7) << 4);
 }
 
 __device__ __forceinline__ uint4 mask_tail(uint4 v, int64_t valid) {
-  // keep bytes [0, valid), zero the rest (valid in [0, 16])
-  if (valid >= 16) return v;
+  // keep bytes [0, valid), zero the rest; branch-free
   uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t lo = 4 * q;
-    if (valid <= lo)
-      w[q] = 0u;
-    else if (valid < lo + 4)
-      w[q] &= (1u << (8 * (valid - lo))) - 1u;
+    const int64_t nb = valid - 4 * q;  // bytes of this dword to keep
+    const int k = nb <= 0 ? 0 : (nb >= 4 ? 4 : int(nb));
+    w[q] &= uint32_t((uint64_t(1) << (8 * k)) - 1u);
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
@@ -101,10 +100,23 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
 
   const int64_t M = g.m, N = g.n, K = g.k;
-  const uint8_t *__restrict__ A = g.a;
-  const uint8_t *__restrict__ B = g.b;
-  const bool mfull = m0 + BM <= M, nfull = n0 + BN <= N;
-  const int KT = int((K + BK - 1) / BK);
+  const int KT = int(K / BK);              // full K tiles
+  const int64_t ktail = K - int64_t(KT) * BK;
+  const int T = KT + (ktail > 0 ? 1 : 0);  // K iterations
+
+  // Per-thread 16-byte chunks of the A and B tiles, as 32-bit byte offsets
+  // from the operand base (the host keeps every operand below 2 GiB).  Rows
+  // past M / N are clamped to the last row: they feed accumulators that are
+  // never stored.  Chunk c of a thread sits RS rows below chunk 0 and, the
+  // swizzle depending only on row / 2 mod 8, RS * BK bytes further in LDS.
+  constexpr int RS = NT / 8;
+  const int r0 = tid >> 3, ch0 = tid & 7;
+  uint32_t oa[ACH], ob[BCH];
+#pragma unroll
+  for (int c = 0; c < ACH; ++c) oa[c] = uint32_t(min(m0 + c * RS + r0, M - 1) * g.lda) + ch0 * 16;
+#pragma unroll
+  for (int c = 0; c < BCH; ++c) ob[c] = uint32_t(min(n0 + c * RS + r0, N - 1) * g.ldb) + ch0 * 16;
+  const uint32_t l0 = lds_off(r0, ch0);
 
   v4f acc[FI][FJ];
 #pragma unroll
@@ -113,81 +125,91 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
     for (int j = 0; j < FJ; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
   uint4 ra[ACH], rb[BCH];
+  const uint8_t *__restrict__ A = g.a;
+  const uint8_t *__restrict__ B = g.b;
 
+  // full K tile: no bounds checks at all
   auto gload = [&](int kt) {
-    const int64_t k0 = int64_t(kt) * BK;
-    const bool kfull = k0 + BK <= K;
+    const uint32_t k0 = uint32_t(kt) * BK;
 #pragma unroll
-    for (int c = 0; c < ACH; ++c) {
-      const int q = c * NT + tid, row = q >> 3, ch = q & 7;
-      const int64_t gr = m0 + row, gk = k0 + ch * 16;
-      if ((mfull || gr < M) && (kfull || gk < K)) {
-        uint4 v = *reinterpret_cast<const uint4 *>(A + gr * g.lda + gk);
-        ra[c] = kfull ? v : mask_tail(v, K - gk);
-      } else {
-        ra[c] = make_uint4(0u, 0u, 0u, 0u);
-      }
-    }
+    for (int c = 0; c < ACH; ++c) ra[c] = *reinterpret_cast<const uint4 *>(A + (oa[c] + k0));
 #pragma unroll
-    for (int c = 0; c < BCH; ++c) {
-      const int q = c * NT + tid, row = q >> 3, ch = q & 7;
-      const int64_t gr = n0 + row, gk = k0 + ch * 16;
-      if ((nfull || gr < N) && (kfull || gk < K)) {
-        uint4 v = *reinterpret_cast<const uint4 *>(B + gr * g.ldb + gk);
-        rb[c] = kfull ? v : mask_tail(v, K - gk);
-      } else {
-        rb[c] = make_uint4(0u, 0u, 0u, 0u);
-      }
-    }
+    for (int c = 0; c < BCH; ++c) rb[c] = *reinterpret_cast<const uint4 *>(B + (ob[c] + k0));
+  };
+  // the last, partial K tile: bytes at or past K are zero
+  auto gload_tail = [&]() {
+    const uint32_t k0 = uint32_t(KT) * BK;
+    const int64_t gk = int64_t(k0) + ch0 * 16;
+#pragma unroll
+    for (int c = 0; c < ACH; ++c)
+      ra[c] = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(A + (oa[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int c = 0; c < BCH; ++c)
+      rb[c] = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(B + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+  };
+  auto load = [&](int t) {
+    if (t < KT)
+      gload(t);
+    else
+      gload_tail();
   };
 
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int c = 0; c < ACH; ++c) {
-      const int q = c * NT + tid, row = q >> 3, ch = q & 7;
-      *reinterpret_cast<uint4 *>(&sA[buf][lds_off(row, ch)]) = ra[c];
-    }
+    for (int c = 0; c < ACH; ++c) *reinterpret_cast<uint4 *>(&sA[buf][l0 + c * RS * BK]) = ra[c];
 #pragma unroll
-    for (int c = 0; c < BCH; ++c) {
-      const int q = c * NT + tid, row = q >> 3, ch = q & 7;
-      *reinterpret_cast<uint4 *>(&sB[buf][lds_off(row, ch)]) = rb[c];
-    }
+    for (int c = 0; c < BCH; ++c) *reinterpret_cast<uint4 *>(&sB[buf][l0 + c * RS * BK]) = rb[c];
   };
 
-  auto frag = [&](const uint8_t *base, int row) -> v8i {
-    const int gq = lane >> 4;
-    const uint4 lo = *reinterpret_cast<const uint4 *>(base + lds_off(row, 2 * gq));
-    const uint4 hi = *reinterpret_cast<const uint4 *>(base + lds_off(row, 2 * gq + 1));
+  // Fragment reads.  Lane l of a 16-row fragment reads row (l & 15) of it,
+  // 16-byte chunks 2(l >> 4) and 2(l >> 4) + 1.  Fragment rows start at
+  // multiples of 16, so the swizzle term (row >> 1) & 7 depends on l only and
+  // fragment f of a wave sits exactly 16 * 128 * f bytes after fragment 0:
+  // two per-lane base offsets (low / high chunk) serve every fragment.
+  const int fr = lane & 15, fq = lane >> 4;
+  const uint32_t f_lo = uint32_t(fr) * BK + (uint32_t((2 * fq) ^ (fr >> 1)) & 7) * 16;
+  const uint32_t f_hi = uint32_t(fr) * BK + (uint32_t((2 * fq + 1) ^ (fr >> 1)) & 7) * 16;
+  auto frag = [&](const uint8_t *base) -> v8i {
+    const uint4 lo = *reinterpret_cast<const uint4 *>(base + f_lo);
+    const uint4 hi = *reinterpret_cast<const uint4 *>(base + f_hi);
     return v8i{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
   };
 
+  // A fragments are read one step ahead of the MFMAs that consume them, so the
+  // LDS latency of fragment i+1 hides behind the FJ MFMAs of fragment i.
   auto compute = [&](int buf) {
+    const uint8_t *a_s = &sA[buf][wm * TM * BK];
+    const uint8_t *b_s = &sB[buf][wn * TN * BK];
     v8i bfr[FJ];
 #pragma unroll
-    for (int j = 0; j < FJ; ++j) bfr[j] = frag(sB[buf], wn * TN + j * 16 + (lane & 15));
+    for (int j = 0; j < FJ; ++j) bfr[j] = frag(b_s + j * 16 * BK);
+    v8i acur = frag(a_s);
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
-      const v8i afr = frag(sA[buf], wm * TM + i * 16 + (lane & 15));
+      v8i anext = acur;
+      if (i + 1 < FI) anext = frag(a_s + (i + 1) * 16 * BK);
 #pragma unroll
       for (int j = 0; j < FJ; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfr[j], afr, acc[i][j], FB, FA, 0, 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfr[j], acur, acc[i][j], FB, FA, 0, 0, 0, 0);
+      acur = anext;
     }
   };
 
-  if (KT > 0) {
-    gload(0);
+  if (T > 0) {
+    load(0);
     sstore(0);
     __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      if (kt + 1 < KT) gload(kt + 1);
-      compute(kt & 1);
-      if (kt + 1 < KT) sstore((kt + 1) & 1);
+    for (int t = 0; t < T; ++t) {
+      if (t + 1 < T) load(t + 1);
+      compute(t & 1);
+      if (t + 1 < T) sstore((t + 1) & 1);
       __syncthreads();
     }
   }
 
   // epilogue: lane holds rows (lane & 15), columns 4*(lane >> 4) .. +3 of each 16x16 block
   const int e = pow2_exponent(g.a_scale_inv) + pow2_exponent(g.b_scale_inv);
+  const bool mfull = m0 + BM <= M, nfull = n0 + BN <= N;
 #pragma unroll
   for (int i = 0; i < FI; ++i) {
     const int64_t row = m0 + wm * TM + i * 16 + (lane & 15);
@@ -254,7 +276,45 @@ hipError_t launch_fmts(const GemmParams &g, hipStream_t s) {
 
 hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
-  return launch_fmts<256, 256, 2, 2>(g, s);
+  // The kernel addresses each operand with 32-bit offsets: split any operand
+  // of 2 GiB or more into row blocks (independent GEMMs on disjoint outputs).
+  constexpr int64_t kLim = int64_t(1) << 31;
+  const int64_t cbytes = g.out == 1 ? 2 : 4;
+  if (g.m * g.lda >= kLim) {
+    const int64_t rows = (kLim - 1) / g.lda / 256 * 256;
+    for (int64_t r = 0; r < g.m; r += rows) {
+      GemmParams sub = g;
+      sub.a = g.a + r * g.lda;
+      sub.m = g.m - r < rows ? g.m - r : rows;
+      sub.c = static_cast<char *>(g.c) + r * g.ldc * cbytes;
+      const hipError_t e = launch_gemm(sub, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  if (g.n * g.ldb >= kLim) {
+    const int64_t cols = (kLim - 1) / g.ldb / 256 * 256;
+    for (int64_t c0 = 0; c0 < g.n; c0 += cols) {
+      GemmParams sub = g;
+      sub.b = g.b + c0 * g.ldb;
+      sub.n = g.n - c0 < cols ? g.n - c0 : cols;
+      sub.c = static_cast<char *>(g.c) + c0 * cbytes;
+      const hipError_t e = launch_gemm(sub, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  // Tile choice by wave quantization: each CU runs one workgroup at a time, so
+  // a grid costs ceil(tiles / CUs) rounds of one tile's time.  A 256 x 128
+  // tile takes ~0.57 of a 256 x 256 tile (measured on MI355X; it is less
+  // efficient per FLOP), so it wins when the 256 x 256 grid leaves the last
+  // round mostly empty (e.g. N = 6144: 384 tiles, 1.5 rounds).
+  const int64_t t256 = ((g.m + 255) / 256) * ((g.n + 255) / 256);
+  const int64_t t128 = ((g.m + 255) / 256) * ((g.n + 127) / 128);
+  const double c256 = double((t256 + kCUs - 1) / kCUs);
+  const double c128 = 0.57 * double((t128 + kCUs - 1) / kCUs);
+  if (c128 < c256) return launch_fmts<256, 128, 4, 2>(g, s);
+  return launch_fmts<256, 256, 2, 4>(g, s);
 }
 
 }  // namespace qe

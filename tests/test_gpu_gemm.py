@@ -139,3 +139,25 @@ def test_k_zero_and_empty():
                    c_init=np.full(32, 3.0, dtype=np.float32))
     np.testing.assert_array_equal(got, np.full(32, 3.0, dtype=np.float32))
     assert qe.qe_fp8_gemm_tn(0, 0, 16, 0, 0, 16, 0, 4, 16, 0, 0, 0, qe.F32, 4) == "OK"
+
+
+@pytest.mark.parametrize("shape", [(4096, 4096, 1024), (4096, 6144, 1024), (4100, 4100, 1040)], ids=str)
+def test_large_grids_bit_exact(shape):
+    """Grids large enough to select each macro-tile shape (256 x 256 when the
+    grid fills whole rounds of CUs, 256 x 128 otherwise), integer operands so
+    the result is exact."""
+    qe = need_lib()
+    d = dev()
+    m, n, k = shape
+    g = torch.Generator(device=d)
+    g.manual_seed(11)
+    ai = torch.randint(-6, 7, (m, k), device=d, generator=g)
+    bi = torch.randint(-6, 7, (n, k), device=d, generator=g)
+    lut = torch.from_numpy(fp8.encode(np.arange(-6, 7, dtype=np.float64), "E4M3")).to(d)
+    a_t = lut[(ai + 6)].contiguous()
+    b_t = lut[(bi + 6)].contiguous()
+    s = torch.tensor([1.0, 1.0], dtype=torch.float32, device=d)
+    c = torch.empty((m, n), dtype=torch.float32, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, k, b_t, 0, k, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+    ref = (ai.double() @ bi.double().T).float()
+    assert torch.equal(c, ref)
