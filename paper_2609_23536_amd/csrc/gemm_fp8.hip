@@ -10,13 +10,21 @@
 // it to an FP32 destination in place: the direct placement of dW into its
 // slice of the flat main-gradient buffer (§3.4), with no staging copy.
 //
-// Kernel: BM x BN x 128 macro-tile per workgroup, 64-wide waves on a WM x WN
-// grid, each wave owning a (BM/WM) x (BN/WN) sub-tile accumulated with
+// Kernel: BM x BN x 128 macro-tile per workgroup, eight 64-wide waves on a
+// WM x WN grid, each wave owning a (BM/WM) x (BN/WN) sub-tile accumulated with
 // v_mfma_f32_16x16x128_f8f6f4 (operand formats chosen per call: E4M3 or
-// E5M2).  K tiles are staged through LDS, double-buffered, loaded with
-// 16-byte global loads into registers one tile ahead of the MFMA work.  LDS
-// rows are 128 bytes; their 16-byte chunks are XOR-swizzled by (row/2) mod 8
-// so the 16 rows read by one fragment load hit all 64 banks once.
+// E5M2).  K tiles are double-buffered in LDS and filled by LDS-bound global
+// loads (global_load_lds_dwordx4: no register staging, no LDS store
+// instructions) issued one K tile ahead; each wave waits for its own loads
+// and a barrier publishes the stage.  LDS rows are 128 bytes; their 16-byte
+// chunks are XOR-swizzled by (row/2) mod 8 so the 16 rows read by one fragment
+// load hit all 64 banks once, and since a fragment starts on a multiple of 16
+// rows, every fragment of a wave is one base address plus a constant.
+// The LDS-bound loads are written as inline assembly: the compiler's own
+// form makes it wait for them before every LDS read, serialising the loads
+// with the MFMA work.  Rows past M / N are clamped to the last row (their
+// results are never stored), so only the last, partial K tile needs masking;
+// it goes through registers.
 //
 // MFMA operand order: the B fragment is passed as source A and the A fragment
 // as source B, so each lane ends up holding four consecutive output columns of
@@ -81,15 +89,15 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   constexpr int BCH = BN * (BK / 16) / NT;
   static_assert(ACH * NT == BM * (BK / 16) && BCH * NT == BN * (BK / 16), "tile / thread mismatch");
 
-  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BN * BK];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BN) * BK];
+  constexpr int NW = WM * WN;
+  constexpr int STAGE = (BM + BN) * BK;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
-  // tile coordinates: XCD-contiguous, then grouped along M
   const int pid = xcd_remap(blockIdx.x, tiles_m * tiles_n);
   const int in_group = kGroupM * tiles_n;
   const int group = pid / in_group;
@@ -100,23 +108,29 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
 
   const int64_t M = g.m, N = g.n, K = g.k;
-  const int KT = int(K / BK);              // full K tiles
+  const int KT = int(K / BK);
   const int64_t ktail = K - int64_t(KT) * BK;
-  const int T = KT + (ktail > 0 ? 1 : 0);  // K iterations
+  const int T = KT + (ktail > 0 ? 1 : 0);
 
-  // Per-thread 16-byte chunks of the A and B tiles, as 32-bit byte offsets
-  // from the operand base (the host keeps every operand below 2 GiB).  Rows
-  // past M / N are clamped to the last row: they feed accumulators that are
-  // never stored.  Chunk c of a thread sits RS rows below chunk 0 and, the
-  // swizzle depending only on row / 2 mod 8, RS * BK bytes further in LDS.
-  constexpr int RS = NT / 8;
-  const int r0 = tid >> 3, ch0 = tid & 7;
+  // LDS-bound loads: each wave instruction fills one contiguous 1 KB block
+  // (8 rows x 128 B), lane l writing bytes 16l..16l+15; lane l fetches the
+  // global chunk that the swizzle puts at row 8b + l/8, physical chunk l % 8.
+  const int lrow = lane >> 3;
   uint32_t oa[ACH], ob[BCH];
 #pragma unroll
-  for (int c = 0; c < ACH; ++c) oa[c] = uint32_t(min(m0 + c * RS + r0, M - 1) * g.lda) + ch0 * 16;
+  for (int c = 0; c < ACH; ++c) {
+    const int row = 8 * (wave + NW * c) + lrow;
+    const int lch = (lane & 7) ^ ((row >> 1) & 7);
+    oa[c] = uint32_t(min(m0 + row, M - 1) * g.lda) + lch * 16;
+  }
 #pragma unroll
-  for (int c = 0; c < BCH; ++c) ob[c] = uint32_t(min(n0 + c * RS + r0, N - 1) * g.ldb) + ch0 * 16;
-  const uint32_t l0 = lds_off(r0, ch0);
+  for (int c = 0; c < BCH; ++c) {
+    const int row = 8 * (wave + NW * c) + lrow;
+    const int lch = (lane & 7) ^ ((row >> 1) & 7);
+    ob[c] = uint32_t(min(n0 + row, N - 1) * g.ldb) + lch * 16;
+  }
+  const uint32_t lds_base = uint32_t(reinterpret_cast<uintptr_t>(smem));
+  const uint32_t wblk = __builtin_amdgcn_readfirstlane(lds_base + uint32_t(wave) * 1024u);
 
   v4f acc[FI][FJ];
 #pragma unroll
@@ -124,48 +138,46 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
 #pragma unroll
     for (int j = 0; j < FJ; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra[ACH], rb[BCH];
-  const uint8_t *__restrict__ A = g.a;
-  const uint8_t *__restrict__ B = g.b;
-
-  // full K tile: no bounds checks at all
-  auto gload = [&](int kt) {
-    const uint32_t k0 = uint32_t(kt) * BK;
-#pragma unroll
-    for (int c = 0; c < ACH; ++c) ra[c] = *reinterpret_cast<const uint4 *>(A + (oa[c] + k0));
-#pragma unroll
-    for (int c = 0; c < BCH; ++c) rb[c] = *reinterpret_cast<const uint4 *>(B + (ob[c] + k0));
-  };
-  // the last, partial K tile: bytes at or past K are zero
-  auto gload_tail = [&]() {
-    const uint32_t k0 = uint32_t(KT) * BK;
-    const int64_t gk = int64_t(k0) + ch0 * 16;
+  auto issue_full = [&](int kt, int buf) {
+    const uint8_t *ga = g.a + int64_t(kt) * BK;
+    const uint8_t *gb = g.b + int64_t(kt) * BK;
+    const uint32_t sa = wblk + uint32_t(buf * STAGE);
+    const uint32_t sb = sa + uint32_t(BM * BK);
 #pragma unroll
     for (int c = 0; c < ACH; ++c)
-      ra[c] = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(A + (oa[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[c]), "s"(ga),
+                   "s"(sa + uint32_t(c * NW * 1024)) : "memory", "m0");
 #pragma unroll
     for (int c = 0; c < BCH; ++c)
-      rb[c] = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(B + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[c]), "s"(gb),
+                   "s"(sb + uint32_t(c * NW * 1024)) : "memory", "m0");
   };
-  auto load = [&](int t) {
+  auto issue_tail = [&](int buf) {
+    uint8_t *dA = smem + buf * STAGE;
+    uint8_t *dB = dA + BM * BK;
+    const uint32_t k0 = uint32_t(KT) * BK;
+#pragma unroll
+    for (int c = 0; c < ACH; ++c) {
+      const int row = 8 * (wave + NW * c) + lrow;
+      const int64_t gk = int64_t(k0) + (((lane & 7) ^ ((row >> 1) & 7)) * 16);
+      const uint4 v = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.a + (oa[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4 *>(dA + (wave + NW * c) * 1024 + lane * 16) = v;
+    }
+#pragma unroll
+    for (int c = 0; c < BCH; ++c) {
+      const int row = 8 * (wave + NW * c) + lrow;
+      const int64_t gk = int64_t(k0) + (((lane & 7) ^ ((row >> 1) & 7)) * 16);
+      const uint4 v = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.b + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4 *>(dB + (wave + NW * c) * 1024 + lane * 16) = v;
+    }
+  };
+  auto issue = [&](int t, int buf) {
     if (t < KT)
-      gload(t);
+      issue_full(t, buf);
     else
-      gload_tail();
+      issue_tail(buf);
   };
 
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < ACH; ++c) *reinterpret_cast<uint4 *>(&sA[buf][l0 + c * RS * BK]) = ra[c];
-#pragma unroll
-    for (int c = 0; c < BCH; ++c) *reinterpret_cast<uint4 *>(&sB[buf][l0 + c * RS * BK]) = rb[c];
-  };
-
-  // Fragment reads.  Lane l of a 16-row fragment reads row (l & 15) of it,
-  // 16-byte chunks 2(l >> 4) and 2(l >> 4) + 1.  Fragment rows start at
-  // multiples of 16, so the swizzle term (row >> 1) & 7 depends on l only and
-  // fragment f of a wave sits exactly 16 * 128 * f bytes after fragment 0:
-  // two per-lane base offsets (low / high chunk) serve every fragment.
   const int fr = lane & 15, fq = lane >> 4;
   const uint32_t f_lo = uint32_t(fr) * BK + (uint32_t((2 * fq) ^ (fr >> 1)) & 7) * 16;
   const uint32_t f_hi = uint32_t(fr) * BK + (uint32_t((2 * fq + 1) ^ (fr >> 1)) & 7) * 16;
@@ -175,11 +187,9 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
     return v8i{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
   };
 
-  // A fragments are read one step ahead of the MFMAs that consume them, so the
-  // LDS latency of fragment i+1 hides behind the FJ MFMAs of fragment i.
   auto compute = [&](int buf) {
-    const uint8_t *a_s = &sA[buf][wm * TM * BK];
-    const uint8_t *b_s = &sB[buf][wn * TN * BK];
+    const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
+    const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
     v8i bfr[FJ];
 #pragma unroll
     for (int j = 0; j < FJ; ++j) bfr[j] = frag(b_s + j * 16 * BK);
@@ -195,15 +205,18 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
     }
   };
 
-  if (T > 0) {
-    load(0);
-    sstore(0);
+  auto stage_sync = [&]() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+
+  if (T > 0) {
+    issue(0, 0);
+    stage_sync();
     for (int t = 0; t < T; ++t) {
-      if (t + 1 < T) load(t + 1);
+      if (t + 1 < T) issue(t + 1, (t + 1) & 1);
       compute(t & 1);
-      if (t + 1 < T) sstore((t + 1) & 1);
-      __syncthreads();
+      stage_sync();
     }
   }
 
