@@ -9,10 +9,11 @@
 // Q rounds to nearest even and saturates to +-fmax; NaN becomes 0x7F with the
 // input's sign bit.  Formats: OCP E4M3 (max 448) and E5M2 (max 57344).
 //
-// Layout: one workgroup of 256 lanes per 128 x 128 tile.  Phase 1: eight lanes
-// cover one 128-element row segment with 16-byte loads (bf16: 2, fp32: 4 per
-// lane), convert 16 values to one 16-byte code vector, store it row-wise and
-// into an LDS tile whose 16-byte chunks are XOR-swizzled by row block.
+// Layout: one workgroup of 256 lanes per 128 x 128 tile.  Phase 1: every load
+// instruction is one contiguous 16-byte piece per lane along a row (16 lanes
+// per bf16 row, 32 per fp32 row); each lane converts its 8 (or 4) values and
+// stores the codes row-wise and into an LDS tile whose 16-byte chunks are
+// XOR-swizzled by row block.
 // Phase 2: each lane gathers a 16-row x 4-column block of codes from LDS and
 // writes four 16-byte column segments; eight consecutive lanes complete one
 // 128-byte run of a transposed row.  amax: a max over the |x| bit patterns
@@ -29,22 +30,17 @@ constexpr int kThreads = 256;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t nan_fix(uint32_t u, int byte, float v) {
-  if (v != v) {
-    uint32_t code = 0x7fu | ((__float_as_uint(v) >> 24) & 0x80u);
-    u = (u & ~(0xffu << (8 * byte))) | (code << (8 * byte));
-  }
-  return u;
-}
-
-// Four scaled values -> four FP8 codes, byte i = value i.
+// Four scaled values -> four FP8 codes, byte i = value i.  The hardware
+// conversion rounds to nearest even but neither saturates (it overflows to
+// NaN / inf) nor keeps the sign of a NaN, so values are clamped first with
+// med3, which maps NaN to -fmax; NaN inputs are repaired separately.
 template <int FMT>
 __device__ __forceinline__ uint32_t enc4(float a, float b, float c, float d) {
   constexpr float fm = FMT == 0 ? 448.0f : 57344.0f;
-  const float ca = fminf(fmaxf(a, -fm), fm);
-  const float cb = fminf(fmaxf(b, -fm), fm);
-  const float cc = fminf(fmaxf(c, -fm), fm);
-  const float cd = fminf(fmaxf(d, -fm), fm);
+  const float ca = __builtin_amdgcn_fmed3f(a, -fm, fm);
+  const float cb = __builtin_amdgcn_fmed3f(b, -fm, fm);
+  const float cc = __builtin_amdgcn_fmed3f(c, -fm, fm);
+  const float cd = __builtin_amdgcn_fmed3f(d, -fm, fm);
   int r;
   if constexpr (FMT == 0) {
     r = __builtin_amdgcn_cvt_pk_fp8_f32(ca, cb, 0, false);
@@ -53,12 +49,14 @@ __device__ __forceinline__ uint32_t enc4(float a, float b, float c, float d) {
     r = __builtin_amdgcn_cvt_pk_bf8_f32(ca, cb, 0, false);
     r = __builtin_amdgcn_cvt_pk_bf8_f32(cc, cd, r, true);
   }
-  uint32_t u = uint32_t(r);
-  if (__builtin_expect((a != a) | (b != b) | (c != c) | (d != d), 0)) {
-    u = nan_fix(u, 0, a);
-    u = nan_fix(u, 1, b);
-    u = nan_fix(u, 2, c);
-    u = nan_fix(u, 3, d);
+  return uint32_t(r);
+}
+
+// NaN -> 0x7F with the input's sign bit, for the rare thread that saw one.
+__device__ __forceinline__ uint32_t nan_fix(uint32_t u, int byte, float v) {
+  if (v != v) {
+    const uint32_t code = 0x7fu | ((__float_as_uint(v) >> 24) & 0x80u);
+    u = (u & ~(0xffu << (8 * byte))) | (code << (8 * byte));
   }
   return u;
 }
@@ -67,33 +65,37 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as
 
 __device__ __forceinline__ uint32_t abs_bits(float v) { return __float_as_uint(v) & 0x7fffffffu; }
 
-// 16 floats -> 16 codes (+ running amax)
-template <int FMT>
-__device__ __forceinline__ uint4 encode16(const float (&f)[16], float scale, uint32_t &amax) {
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    uint32_t b = abs_bits(f[e]);
-    amax = b > amax ? b : amax;
-  }
-  uint4 q;
-  q.x = enc4<FMT>(f[0] * scale, f[1] * scale, f[2] * scale, f[3] * scale);
-  q.y = enc4<FMT>(f[4] * scale, f[5] * scale, f[6] * scale, f[7] * scale);
-  q.z = enc4<FMT>(f[8] * scale, f[9] * scale, f[10] * scale, f[11] * scale);
-  q.w = enc4<FMT>(f[12] * scale, f[13] * scale, f[14] * scale, f[15] * scale);
-  return q;
-}
-
 __device__ __forceinline__ uint32_t lds_chunk_offset(int row, int chunk) {
   return uint32_t(row) * kTile + (uint32_t((chunk ^ (row >> 4)) & 7) << 4);
 }
 
 __device__ __forceinline__ uint32_t byte_of(uint32_t w, int j) { return (w >> (8 * j)) & 0xffu; }
 
+// E values of one 16-byte input load (8 bf16 or 4 fp32), as floats
+template <bool BF16>
+__device__ __forceinline__ void unpack16(const uint4 &v, float *f) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (BF16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = bf16_to_f32(w[e] & 0xffffu);
+      f[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(w[e]);
+  }
+}
+
 template <bool BF16, int FMT>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64_t tiles_c, int aligned) {
   __shared__ __attribute__((aligned(16))) uint8_t tile[kTile * kTile];
   __shared__ uint32_t red[kThreads / 64];
-  constexpr int kVec = BF16 ? 2 : 4;  // 16-byte loads per 16 elements
+  // Phase 1 mapping: one 16-byte load per lane per step, consecutive lanes on
+  // consecutive 16 bytes of a row (LPR lanes per 128-element row).
+  constexpr int EPL = BF16 ? 8 : 4;          // elements per load
+  constexpr int LPR = kTile / EPL;           // lanes per tile row
+  constexpr int NLD = kTile * kTile / (EPL * kThreads);  // loads per lane
   const int tid = threadIdx.x;
   const int64_t t = blockIdx.x;
   const int64_t r0 = (t / tiles_c) * kTile;
@@ -104,45 +106,51 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64
   uint32_t amax = 0;
 
   if (full) {
-    uint4 raw[4][kVec];
+    uint4 raw[NLD];
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int q = it * kThreads + tid, row = q >> 3, cc = q & 7;
-      const int64_t eoff = (r0 + row) * p.cols + c0 + cc * 16;
-      const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const char *>(p.in) + eoff * (BF16 ? 2 : 4));
+    for (int it = 0; it < NLD; ++it) {
+      const int q = it * kThreads + tid, row = q / LPR, cl = q % LPR;
+      const int64_t eoff = (r0 + row) * p.cols + c0 + cl * EPL;
+      const u32x4 x = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4 *>(static_cast<const char *>(p.in) + eoff * (BF16 ? 2 : 4)));
+      raw[it] = make_uint4(x.x, x.y, x.z, x.w);
+    }
+    uint32_t codes[NLD][EPL / 4];
 #pragma unroll
-      for (int v = 0; v < kVec; ++v) {
-        const u32x4 x = __builtin_nontemporal_load(src + v);
-        raw[it][v] = make_uint4(x.x, x.y, x.z, x.w);
+    for (int it = 0; it < NLD; ++it) {
+      float f[EPL];
+      unpack16<BF16>(raw[it], f);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const uint32_t b = abs_bits(f[e]);
+        amax = b > amax ? b : amax;
+      }
+#pragma unroll
+      for (int w = 0; w < EPL / 4; ++w)
+        codes[it][w] = enc4<FMT>(f[4 * w] * scale, f[4 * w + 1] * scale, f[4 * w + 2] * scale, f[4 * w + 3] * scale);
+    }
+    if (__builtin_expect(amax > 0x7f800000u, 0)) {  // this lane saw a NaN
+#pragma unroll
+      for (int it = 0; it < NLD; ++it) {
+        float f[EPL];
+        unpack16<BF16>(raw[it], f);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) codes[it][e / 4] = nan_fix(codes[it][e / 4], e % 4, f[e]);
       }
     }
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int q = it * kThreads + tid, row = q >> 3, cc = q & 7;
-      float f[16];
+    for (int it = 0; it < NLD; ++it) {
+      const int q = it * kThreads + tid, row = q / LPR, cl = q % LPR;
+      const int col = cl * EPL;
+      const uint32_t lofs = lds_chunk_offset(row, col >> 4) + (col & 15);
       if constexpr (BF16) {
-#pragma unroll
-        for (int v = 0; v < 2; ++v) {
-          const uint32_t w[4] = {raw[it][v].x, raw[it][v].y, raw[it][v].z, raw[it][v].w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            f[v * 8 + 2 * e] = bf16_to_f32(w[e] & 0xffffu);
-            f[v * 8 + 2 * e + 1] = bf16_to_f32(w[e] >> 16);
-          }
-        }
+        if (p.q_row != nullptr)
+          *reinterpret_cast<uint2 *>(p.q_row + (r0 + row) * p.ld_row + c0 + col) = make_uint2(codes[it][0], codes[it][1]);
+        *reinterpret_cast<uint2 *>(tile + lofs) = make_uint2(codes[it][0], codes[it][1]);
       } else {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          f[4 * v + 0] = __uint_as_float(raw[it][v].x);
-          f[4 * v + 1] = __uint_as_float(raw[it][v].y);
-          f[4 * v + 2] = __uint_as_float(raw[it][v].z);
-          f[4 * v + 3] = __uint_as_float(raw[it][v].w);
-        }
+        if (p.q_row != nullptr) *reinterpret_cast<uint32_t *>(p.q_row + (r0 + row) * p.ld_row + c0 + col) = codes[it][0];
+        *reinterpret_cast<uint32_t *>(tile + lofs) = codes[it][0];
       }
-      const uint4 codes = encode16<FMT>(f, scale, amax);
-      if (p.q_row != nullptr)
-        *reinterpret_cast<uint4 *>(p.q_row + (r0 + row) * p.ld_row + c0 + cc * 16) = codes;
-      *reinterpret_cast<uint4 *>(tile + lds_chunk_offset(row, cc)) = codes;
     }
   } else {
     for (int it = 0; it < 4; ++it) {
@@ -160,17 +168,24 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64
             v = static_cast<const float *>(p.in)[r * p.cols + c];
         }
         f[e] = v;
+        const uint32_t b = abs_bits(v);
+        amax = b > amax ? b : amax;
       }
-      const uint4 codes = encode16<FMT>(f, scale, amax);
+      uint32_t w[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        w[k] = enc4<FMT>(f[4 * k] * scale, f[4 * k + 1] * scale, f[4 * k + 2] * scale, f[4 * k + 3] * scale);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[k] = nan_fix(w[k], e, f[4 * k + e]);
+      }
       if (p.q_row != nullptr && r < p.rows) {
-        const uint32_t w[4] = {codes.x, codes.y, codes.z, codes.w};
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int64_t c = c0 + cc * 16 + e;
           if (c < p.cols) p.q_row[r * p.ld_row + c] = uint8_t(byte_of(w[e >> 2], e & 3));
         }
       }
-      *reinterpret_cast<uint4 *>(tile + lds_chunk_offset(row, cc)) = codes;
+      *reinterpret_cast<uint4 *>(tile + lds_chunk_offset(row, cc)) = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
 
