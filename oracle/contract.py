@@ -1,17 +1,17 @@
 """The bookkeeping contract of a pipeline stage, as a plain state machine.
 
-Written from §3 ("QEffect Contract"), Algorithm 1 (§4.1), §4.3 and §4.5 of the
+Written from §3 (the contract), Algorithm 1 (§4.1), §4.3 and §4.5 of the
 paper, and Table "faults".  Every action is *checked* first; a rejected call
-changes nothing (§4.1: a check precedes its physical action, and the
-transition commits only after the action succeeds; Table "faults": a rejected
-stale reference preserves the current record).  Only a failure of the
+changes nothing (§4.1: checks come before the physical work, and the state
+moves only once that work has succeeded; Table "faults": rejecting a stale
+reference leaves the live record intact).  Only a failure of the
 physical action itself aborts the epoch (§4.5).
 
 State:
 * TapeKey K = (e, s, m, u, i): epoch, stage, microbatch, sub-layer unit,
   invocation (§3.1).  A layer is identified by (s, u).
-* Slot pool: one slot per configured microbatch per layer (slot p = m; §4.2 a
-  dW's microbatch index and its reference name the same slot).  Allocating
+* Slot pool: one slot per configured microbatch per layer (slot p = m; §4.2: a
+  dW's explicit microbatch index and its TapeRef must point at one slot).  Allocating
   increments the slot's generation g_p, starting from 0, so the first
   reference is (p, 1); release keeps g_p (§3.1, Invariant 2).
 * Consumer bits {dI, dW}; the slot is released once both have run (§3.1).
