@@ -1,0 +1,130 @@
+"""Full-size parity on the Llama-3-8B-shaped stage in the benchmark's launch
+configuration (graph replay, 4096 tokens, bf16): two steps of F, dI and
+deferred dW for each linear, then
+
+* amax histories and scales bit-exact (the oracle takes the amax of the full
+  tensors, which is cheap);
+* FP8 codes bit-exact on sampled rows of the weight cache and sampled rows of
+  the slot payloads (each is the quantization of a sampled column of X / dY);
+* Y, dX and the placed dW within 1e-3 on a sampled row x column block, which
+  the oracle computes from the quantized sampled rows / columns alone.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import fp8, gemm, scaling
+from tests.gpu_util import dev, dev_bytes, rel_err, torch, upload
+from tests.libqe import need_lib
+
+pytestmark = pytest.mark.gpu
+WL = W.WORKLOADS["llama3_8b_stage_4096tok"]
+
+
+def widen(t):
+    return t.as_f32()
+
+
+@pytest.fixture(scope="module")
+def run():
+    qe = need_lib()
+    d = dev()
+    ctx = qe.Context(1, use_graphs=True)
+    data, outs = [], []
+    grad = torch.zeros(WL.flat_grad_elems(), dtype=torch.float32, device=d)
+    offs = WL.grad_offsets()
+    for u, lin in enumerate(WL.linears):
+        w = W.layer_weight(WL, u)
+        inp = W.layer_inputs(WL, u)
+        dw, dx, ddy = upload(w, d), upload(inp["x"], d), upload(inp["dy"], d)
+        st, L = ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, WL.tokens, dw, qe.BF16, WL.history, WL.margin)
+        assert st == "OK"
+        assert ctx.qe_arena_bind(u, 0, grad, grad.numel(), offs[u], lin.k_in) == "OK"
+        y = torch.empty((WL.tokens, lin.n_out), dtype=torch.int16, device=d)
+        dxo = torch.empty((WL.tokens, lin.k_in), dtype=torch.int16, device=d)
+        data.append((w, inp["x"], inp["dy"], dw, dx, ddy))
+        outs.append((y, dxo))
+    for step in range(2):
+        refs = []
+        for u in range(len(WL.linears)):
+            st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(step, 0, 0, u), data[u][4], qe.BF16, WL.tokens, outs[u][0],
+                                            qe.BF16)
+            assert st == "OK"
+            refs.append(ref)
+        for u in reversed(range(len(WL.linears))):
+            k = qe.key(step, 0, 0, u)
+            assert ctx.qe_fp8_linear_dgrad(u, k, refs[u], data[u][5], qe.BF16, outs[u][1], qe.BF16) == "OK"
+            assert ctx.qe_fp8_linear_wgrad_place(u, k, refs[u], grad, offs[u], WL.linears[u].k_in, qe.INIT) == "OK"
+        if step == 0:
+            assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+    torch.cuda.synchronize()
+    assert ctx.qe_sync() == "OK"
+    yield qe, d, ctx, data, outs, grad
+    ctx.close()
+
+
+def bf16_out(t):
+    return (t.cpu().numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+@pytest.mark.parametrize("u", range(4), ids=[l.name for l in WL.linears])
+def test_layer_fullsize(run, u):
+    qe, d, ctx, data, outs, grad = run
+    lin = WL.linears[u]
+    n, k, t = lin.n_out, lin.k_in, WL.tokens
+    w, x, dy = widen(data[u][0]), widen(data[u][1]), widen(data[u][2])
+    ax, aw, ady = scaling.amax(x), scaling.amax(w), scaling.amax(dy)
+    # the delayed-scaling state after two steps (same inputs each step)
+    sx = scaling.DelayedScaler("E4M3", WL.history, WL.margin)
+    sw = scaling.DelayedScaler("E4M3", WL.history, WL.margin)
+    sdy = scaling.DelayedScaler("E5M2", WL.history, WL.margin)
+    snaps = []
+    for step in range(2):
+        s = {"x": sx.scale_inv, "w": sw.scale_inv, "xs": sx.scale, "ws": sw.scale}
+        sx.record(ax); sw.record(aw); sx.update(); sw.update()
+        s["dy"], s["dys"] = sdy.scale_inv, sdy.scale
+        sdy.record(ady); sdy.update()
+        snaps.append(s)
+    for name, role, ref in (("x", qe.ROLE_X, sx), ("w", qe.ROLE_W, sw), ("dy", qe.ROLE_DY, sdy)):
+        m = ctx.qe_layer_meta(u, role)
+        got = dev_bytes(m.amax_history, 4 * WL.history, d).view(np.float32)
+        np.testing.assert_array_equal(got, ref.hist.astype(np.float32), err_msg=name)
+        assert dev_bytes(m.scale, 4, d).view(np.float32)[0] == ref.scale, name
+    s = snaps[1]                                    # scales the second step quantized with
+    rng = np.random.default_rng(u)
+    I = np.sort(rng.choice(t, 24, replace=False))
+    J = np.sort(rng.choice(n, 24, replace=False))
+    Kk = np.sort(rng.choice(k, 24, replace=False))
+    # codes: weight cache rows, slot payload rows (= sampled columns of X and dY)
+    c = ctx.qe_layer_cache(u)
+    wq = dev_bytes(c["w_q"], n * c["ld_w_q"], d).reshape(n, c["ld_w_q"])[:, :k]
+    np.testing.assert_array_equal(wq[J], gemm.quantize(w[J], s["ws"], "E4M3"))
+    p = ctx.qe_layer_slot_payload(u, 0)
+    xt = dev_bytes(p["x_q_t"], k * p["ld_x_q_t"], d).reshape(k, p["ld_x_q_t"])[:, :t]
+    dyt = dev_bytes(p["dy_q_t"], n * p["ld_dy_q_t"], d).reshape(n, p["ld_dy_q_t"])[:, :t]
+    np.testing.assert_array_equal(xt[Kk], gemm.quantize(x[:, Kk].T, s["xs"], "E4M3"))
+    np.testing.assert_array_equal(dyt[J], gemm.quantize(dy[:, J].T, s["dys"], "E5M2"))
+    # Y[I, J] = Xq[I] Wq[J]^T
+    xq_rows = gemm.quantize(x[I], s["xs"], "E4M3")
+    wq_rows = gemm.quantize(w[J], s["ws"], "E4M3")
+    y_ref = gemm.gemm_tn(xq_rows, "E4M3", wq_rows, "E4M3", s["x"], s["w"])
+    assert rel_err(bf16_out(outs[u][0])[np.ix_(I, J)], y_ref) <= 2.0 ** -8 + 1e-3
+    # dX[I, K] = dYq[I] (Wq^T)[K]^T, (Wq^T)[K] = quantized columns K of W
+    dyq_rows = gemm.quantize(dy[I], s["dys"], "E5M2")
+    wq_cols = gemm.quantize(w[:, Kk].T, s["ws"], "E4M3")
+    dx_ref = gemm.gemm_tn(dyq_rows, "E5M2", wq_cols, "E4M3", s["dy"], s["w"])
+    assert rel_err(bf16_out(outs[u][1])[np.ix_(I, Kk)], dx_ref) <= 2.0 ** -8 + 1e-3
+    # dW[J, K] = dYq^T[J] (Xq^T)[K]^T, placed at offset + n * K + k
+    dw_ref = gemm.gemm_tn(gemm.quantize(dy[:, J].T, s["dys"], "E5M2"), "E5M2",
+                          gemm.quantize(x[:, Kk].T, s["xs"], "E4M3"), "E4M3", s["dy"], s["x"])
+    g = grad.cpu().numpy()
+    off = WL.grad_offsets()[u]
+    got = g[off + J[:, None] * k + Kk[None, :]]
+    assert rel_err(got, dw_ref) <= 1e-3
+
+
+def test_tokens_match(run):
+    qe, d, ctx, data, outs, grad = run
+    st = ctx.qe_get_state()
+    assert st["device_token"] == st["token"] == 2 * 2 * len(WL.linears)
+    assert st["replays"] == 2 * 3 * len(WL.linears)
