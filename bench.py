@@ -42,7 +42,40 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes (counter calibration)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama3_8b_stage_4096tok_traffic.txt")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_23536_amd", "csrc", "gemm_fp8.hip")
+
+
+def gemm_traffic_per_launch():
+    """HBM bytes per GEMM launch from the committed counter runs, or None when
+    they were taken on a different GEMM kernel source than the current one."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha:
+        return None
+    return float(kv["gemm_hbm_bytes_per_launch"])
+
+
+def copy_calibration(nbytes):
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}))
 
 
 class StageBench:
@@ -145,6 +178,9 @@ def cpu_baseline(wl, tokens, min_seconds=10.0):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -204,7 +240,8 @@ def main():
                    "amax_history": wl.history, "graphs": use_graphs},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4),
+                     "traffic": gemm_traffic_per_launch(),
                      "kernel": "gemm_tn_kernel (fwd + dI + dW launches)",
                      "avg_launch_us": round(gemm_ms / gemm_n * 1e3, 2), "launches": gemm_n},
         "quantize": {"achieved": round(q_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
