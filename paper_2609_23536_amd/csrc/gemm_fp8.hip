@@ -10,21 +10,31 @@
 // it to an FP32 destination in place: the direct placement of dW into its
 // slice of the flat main-gradient buffer (§3.4), with no staging copy.
 //
-// Kernel: BM x BN x 128 macro-tile per workgroup, eight 64-wide waves on a
-// WM x WN grid, each wave owning a (BM/WM) x (BN/WN) sub-tile accumulated with
-// v_mfma_f32_16x16x128_f8f6f4 (operand formats chosen per call: E4M3 or
-// E5M2).  K tiles are double-buffered in LDS and filled by LDS-bound global
-// loads (global_load_lds_dwordx4: no register staging, no LDS store
-// instructions) issued one K tile ahead; each wave waits for its own loads
-// and a barrier publishes the stage.  LDS rows are 128 bytes; their 16-byte
-// chunks are XOR-swizzled by (row/2) mod 8 so the 16 rows read by one fragment
-// load hit all 64 banks once, and since a fragment starts on a multiple of 16
-// rows, every fragment of a wave is one base address plus a constant.
-// The LDS-bound loads are written as inline assembly: the compiler's own
-// form makes it wait for them before every LDS read, serialising the loads
-// with the MFMA work.  Rows past M / N are clamped to the last row (their
-// results are never stored), so only the last, partial K tile needs masking;
-// it goes through registers.
+// Two kernels share the scheme below.
+//  * gemm_tn_w4_kernel, 256 x 256 x 128 tiles: four waves (one per SIMD) on a
+//    2 x 2 grid, each a 128 x 128 sub-tile of 4 x 4 v_mfma_f32_32x32x64_f8f6f4
+//    blocks.  A K tile is two 64-wide half-steps; one register set of
+//    fragments feeds 16 MFMAs while the other set is read from LDS, and every
+//    fragment read or LDS-bound load is issued right after an MFMA, in a fixed
+//    order (sched_barrier), so the MFMA pipe stays busy in the single wave.
+//    The stage barrier sits between the two half-steps.  The epilogue goes
+//    through LDS so every store instruction writes whole 512-byte row runs.
+//    Larger wave tiles mean less LDS traffic per FLOP than eight waves.
+//  * gemm_tn_kernel, 256 x 128 x 128 tiles: eight waves (two per SIMD) on a
+//    4 x 2 grid with v_mfma_f32_16x16x128_f8f6f4; used when it quantizes better
+//    onto the 256 CUs.
+// Operand formats (E4M3 or E5M2) are chosen per call.  K tiles are
+// double-buffered in LDS and filled by LDS-bound global loads
+// (global_load_lds_dwordx4: no register staging, no LDS store instructions)
+// issued a K tile ahead; each wave waits for its own loads and a barrier
+// publishes the stage.  LDS rows are 128 bytes; their 16-byte chunks are
+// XOR-swizzled by (row/2) mod 8 so a fragment read hits the 64 banks evenly,
+// and since fragments start on multiples of 16 rows, every fragment of a wave
+// is one base address plus a constant.  The LDS-bound loads are inline
+// assembly: the compiler's own form makes it wait for them before every LDS
+// read, serialising the loads with the MFMA work.  Rows past M / N are
+// clamped to the last row (their results are never stored), so only the last,
+// partial K tile needs masking; it goes through registers.
 //
 // MFMA operand order: the B fragment is passed as source A and the A fragment
 // as source B, so each lane ends up holding four consecutive output columns of
@@ -263,6 +273,271 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   }
 }
 
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// 256 x 256 x 128 tile, four waves (one per SIMD) on a 2 x 2 grid, each wave a
+// 128 x 128 sub-tile of 4 x 4 v_mfma_f32_32x32x64_f8f6f4 blocks.  A K tile is
+// two 64-wide half-steps; the fragments of the next half-step are read into a
+// second register set while the 16 MFMAs of the current one run.  The stage
+// barrier sits between the two half-steps of a tile, so the first fragment
+// reads of the next tile overlap the second half-step's MFMAs; LDS-bound loads
+// run two tiles ahead of the MFMAs.
+template <int FA, int FB, int OUT>
+__global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok) {
+  constexpr int BM = 256, BN = 256, NW = 4, TM = 128, TN = 128;
+  constexpr int CH = BM * (BK / 16) / 256;  // 16-byte chunks per lane per operand tile (8)
+  constexpr int STAGE = (BM + BN) * BK;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int pid = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int in_group = kGroupM * tiles_n;
+  const int group = pid / in_group;
+  const int first_m = group * kGroupM;
+  const int gsize = min(tiles_m - first_m, kGroupM);
+  const int tm = first_m + (pid % in_group) % gsize;
+  const int tn = (pid % in_group) / gsize;
+  const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+
+  const int64_t M = g.m, N = g.n, K = g.k;
+  const int KT = int(K / BK);
+  const int64_t ktail = K - int64_t(KT) * BK;
+  const int T = KT + (ktail > 0 ? 1 : 0);
+
+  const int lrow = lane >> 3;
+  uint32_t oa[CH], ob[CH];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int row = 8 * (wave + NW * c) + lrow;
+    const int lch = (lane & 7) ^ ((row >> 1) & 7);
+    oa[c] = uint32_t(min(m0 + row, M - 1) * g.lda) + lch * 16;
+    ob[c] = uint32_t(min(n0 + row, N - 1) * g.ldb) + lch * 16;
+  }
+  const uint32_t lds_base = uint32_t(reinterpret_cast<uintptr_t>(smem));
+  const uint32_t wblk = __builtin_amdgcn_readfirstlane(lds_base + uint32_t(wave) * 1024u);
+
+  auto issue = [&](int kt, int buf) {
+    if (kt < KT) {
+      const uint8_t *ga = g.a + int64_t(kt) * BK;
+      const uint8_t *gb = g.b + int64_t(kt) * BK;
+      const uint32_t sa = wblk + uint32_t(buf * STAGE);
+      const uint32_t sb = sa + uint32_t(BM * BK);
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+        asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[c]), "s"(ga),
+                     "s"(sa + uint32_t(c * NW * 1024)) : "memory", "m0");
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+        asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[c]), "s"(gb),
+                     "s"(sb + uint32_t(c * NW * 1024)) : "memory", "m0");
+    } else {  // the last, partial K tile, through registers: bytes at or past K are zero
+      uint8_t *dA = smem + buf * STAGE;
+      uint8_t *dB = dA + BM * BK;
+      const uint32_t k0 = uint32_t(KT) * BK;
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int row = 8 * (wave + NW * c) + lrow;
+        const int64_t gk = int64_t(k0) + (((lane & 7) ^ ((row >> 1) & 7)) * 16);
+        const uint4 va = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.a + (oa[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+        const uint4 vb = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.b + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
+        *reinterpret_cast<uint4 *>(dA + (wave + NW * c) * 1024 + lane * 16) = va;
+        *reinterpret_cast<uint4 *>(dB + (wave + NW * c) * 1024 + lane * 16) = vb;
+      }
+    }
+  };
+
+  // 32-row fragments: lane l reads row (l & 31), the 32 bytes 32 (l >> 5) .. +31
+  // of the 64-wide half-step h, i.e. chunks 4h + 2 (l >> 5) and the next.  The
+  // swizzle term depends on (l & 31) only, so fragments are base + constant.
+  const int fr = lane & 31, fh = lane >> 5;
+  uint32_t fo[2][2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    fo[h][0] = uint32_t(fr) * BK + (uint32_t((4 * h + 2 * fh) ^ (fr >> 1)) & 7) * 16;
+    fo[h][1] = uint32_t(fr) * BK + (uint32_t((4 * h + 2 * fh + 1) ^ (fr >> 1)) & 7) * 16;
+  }
+  auto frag = [&](const uint8_t *base, int h) -> v8i {
+    const uint4 lo = *reinterpret_cast<const uint4 *>(base + fo[h][0]);
+    const uint4 hi = *reinterpret_cast<const uint4 *>(base + fo[h][1]);
+    return v8i{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+  };
+  auto load_frags = [&](int buf, int h, v8i (&fa)[4], v8i (&fb)[4]) {
+    const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
+    const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[i] = frag(a_s + i * 32 * BK, h);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = frag(b_s + j * 32 * BK, h);
+  };
+
+  v16f acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  auto mfma_all = [&](const v8i (&fa)[4], const v8i (&fb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
+  };
+
+  // One fragment read (or one LDS-bound load) is issued after each MFMA, in
+  // this exact order (sched_barrier), so the single wave per SIMD keeps the
+  // MFMA pipe busy while its memory instructions issue in the MFMA shadow.
+  auto read_one = [&](int buf, int h, int q, v8i (&fa)[4], v8i (&fb)[4]) {
+    // q = 0..7: a0, b0, b1, b2, b3, a1, a2, a3 (the order the MFMAs need them)
+    const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
+    const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
+    if (q == 0) fa[0] = frag(a_s, h);
+    else if (q <= 4) fb[q - 1] = frag(b_s + (q - 1) * 32 * BK, h);
+    else fa[q - 4] = frag(a_s + (q - 4) * 32 * BK, h);
+  };
+  auto dma_one = [&](int kt, int buf, int q) {
+    const uint32_t sa = wblk + uint32_t(buf * STAGE);
+    if (q < CH) {
+      const uint8_t *ga = g.a + int64_t(kt) * BK;
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[q]), "s"(ga),
+                   "s"(sa + uint32_t(q * NW * 1024)) : "memory", "m0");
+    } else {
+      const uint8_t *gb = g.b + int64_t(kt) * BK;
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[q - CH]), "s"(gb),
+                   "s"(sa + uint32_t(BM * BK) + uint32_t((q - CH) * NW * 1024)) : "memory", "m0");
+    }
+  };
+  auto mfma_one = [&](int q, const v8i (&fa)[4], const v8i (&fb)[4]) {
+    const int i = q >> 2, j = q & 3;
+    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
+  };
+
+  if (T > 0) {
+    v8i a0[4], b0[4], a1[4], b1[4];
+    issue(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    load_frags(0, 0, a0, b0);
+    if (T > 1) issue(1, 1);
+    for (int t = 0; t < T; ++t) {
+      const int buf = t & 1;
+      const bool dma = t + 2 < KT;   // full tiles go LDS-bound, interleaved below
+      // first half: MFMAs on set 0, reads of set 1 (second half of tile t)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_one(q, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (q < 8) {
+          read_one(buf, 1, q, a1, b1);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();                     // tile t+1 published; tile t fully read
+      if (t + 2 < T && !dma) issue(t + 2, buf);
+      // second half: MFMAs on set 1, loads of tile t+2, reads of set 0 (tile t+1)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_one(q, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (dma) dma_one(t + 2, buf, q);
+        if (q >= 8 && t + 1 < T) read_one(buf ^ 1, 0, q - 8, a0, b0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // Epilogue through LDS: the 32 x 32 MFMA layout gives each lane one row and
+  // scattered column quads, so store instructions would touch 32 rows x 32 B.
+  // Each wave instead writes one 32-row block of its sub-tile (32 x 128 FP32,
+  // rows padded to 132 floats) into LDS, then reads it back row-contiguous:
+  // 32 lanes x 16 B cover one 512-byte output row run per store instruction.
+  __syncthreads();  // every wave is done reading the last stage
+  constexpr int EP = 132;  // padded row, in floats
+  float *ep = reinterpret_cast<float *>(smem) + wave * 32 * EP;
+  const int e = pow2_exponent(g.a_scale_inv) + pow2_exponent(g.b_scale_inv);
+  const bool nfull = n0 + BN <= N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = j * 32 + 8 * q + 4 * (lane >> 5);
+        *reinterpret_cast<float4 *>(ep + (lane & 31) * EP + col) =
+            make_float4(__builtin_ldexpf(acc[i][j][4 * q], e), __builtin_ldexpf(acc[i][j][4 * q + 1], e),
+                        __builtin_ldexpf(acc[i][j][4 * q + 2], e), __builtin_ldexpf(acc[i][j][4 * q + 3], e));
+      }
+    // same wave writes then reads its own LDS rows: LDS operations of one wave
+    // complete in order
+#pragma unroll 4
+    for (int it = 0; it < 16; ++it) {
+      const int r = 2 * it + (lane >> 5);
+      const int64_t row = m0 + wm * TM + i * 32 + r;
+      const int cl = (lane & 31) * 4;
+      const int64_t col = n0 + wn * TN + cl;
+      const float4 v4 = *reinterpret_cast<const float4 *>(ep + r * EP + cl);
+      if (row >= M) continue;
+      const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+      if (vec_ok && (nfull || col + 4 <= N)) {
+        if constexpr (OUT == 0) {
+          *reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col) = v4;
+        } else if constexpr (OUT == 1) {
+          const uint32_t lo = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
+          const uint32_t hi = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+          *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(g.c) + row * g.ldc + col) = make_uint2(lo, hi);
+        } else {
+          float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col);
+          const float4 o = *dst;
+          *dst = make_float4(o.x + v[0], o.y + v[1], o.z + v[2], o.w + v[3]);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if (col + t >= N) break;
+          if constexpr (OUT == 0) {
+            static_cast<float *>(g.c)[row * g.ldc + col + t] = v[t];
+          } else if constexpr (OUT == 1) {
+            static_cast<uint16_t *>(g.c)[row * g.ldc + col + t] = uint16_t(f32_to_bf16_bits(v[t]));
+          } else {
+            float *dst = static_cast<float *>(g.c) + row * g.ldc + col + t;
+            *dst = *dst + v[t];
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int FA, int FB>
+hipError_t launch_w4(const GemmParams &g, hipStream_t s) {
+  const int tiles_m = int((g.m + 255) / 256), tiles_n = int((g.n + 255) / 256);
+  const uintptr_t cp = reinterpret_cast<uintptr_t>(g.c);
+  const int vec_ok = (g.out == 1) ? (g.ldc % 4 == 0 && cp % 8 == 0) : (g.ldc % 4 == 0 && cp % 16 == 0);
+  const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n)), block(256);
+  switch (g.out) {
+    case 0: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 0>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    case 1: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 1>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    default: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 2>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_w4_fmts(const GemmParams &g, hipStream_t s) {
+  if (g.fmt_a == 0 && g.fmt_b == 0) return launch_w4<0, 0>(g, s);
+  if (g.fmt_a == 1 && g.fmt_b == 0) return launch_w4<1, 0>(g, s);
+  if (g.fmt_a == 0 && g.fmt_b == 1) return launch_w4<0, 1>(g, s);
+  return launch_w4<1, 1>(g, s);
+}
+
 template <int BM, int BN, int WM, int WN, int FA, int FB>
 hipError_t launch_out(const GemmParams &g, hipStream_t s) {
   const int tiles_m = int((g.m + BM - 1) / BM), tiles_n = int((g.n + BN - 1) / BN);
@@ -318,16 +593,16 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
     return hipSuccess;
   }
   // Tile choice by wave quantization: each CU runs one workgroup at a time, so
-  // a grid costs ceil(tiles / CUs) rounds of one tile's time.  A 256 x 128
-  // tile takes ~0.57 of a 256 x 256 tile (measured on MI355X; it is less
-  // efficient per FLOP), so it wins when the 256 x 256 grid leaves the last
-  // round mostly empty (e.g. N = 6144: 384 tiles, 1.5 rounds).
+  // a grid costs ceil(tiles / CUs) rounds of one tile's time.  A round of the
+  // 256 x 128 kernel takes ~0.62 of a round of the 256 x 256 one (measured on
+  // MI355X; it is less efficient per FLOP), so it wins when the 256 x 256 grid
+  // leaves the last round mostly empty (e.g. N = 6144: 384 tiles).
   const int64_t t256 = ((g.m + 255) / 256) * ((g.n + 255) / 256);
   const int64_t t128 = ((g.m + 255) / 256) * ((g.n + 127) / 128);
   const double c256 = double((t256 + kCUs - 1) / kCUs);
-  const double c128 = 0.57 * double((t128 + kCUs - 1) / kCUs);
+  const double c128 = 0.62 * double((t128 + kCUs - 1) / kCUs);
   if (c128 < c256) return launch_fmts<256, 128, 4, 2>(g, s);
-  return launch_fmts<256, 256, 2, 4>(g, s);
+  return launch_w4_fmts(g, s);
 }
 
 }  // namespace qe
