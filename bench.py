@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--workload", default="llama3_8b_stage_4096tok")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the copied-gradient passes (direct placement only)")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
@@ -79,10 +81,10 @@ def copy_calibration(nbytes):
 
 
 class StageBench:
-    def __init__(self, qe, torch, wl, use_graphs, device):
+    def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False):
         import workloads as W
         self.qe, self.torch, self.wl, self.d = qe, torch, wl, device
-        self.ctx = qe.Context(1, use_graphs=use_graphs)
+        self.ctx = qe.Context(1, use_graphs=use_graphs, copy_gradients=copy_gradients)
         self.n_lin = len(wl.linears)
         bf = wl.in_dtype == "bf16"
         self.dt = qe.BF16 if bf else qe.F32
@@ -213,20 +215,51 @@ def main():
     ms = el / args.steps * 1e3
     value = flops / (el / args.steps) / 1e12
 
-    # instrumented eager pass: per-kernel-class times from HIP events on the graph stream
     b.ctx.close()
     del b
     torch.cuda.empty_cache()
-    e = StageBench(qe, torch, wl, False, dev)
-    e.step()
-    torch.cuda.synchronize()
-    e.ctx.qe_set_kernel_timing(True)
-    for _ in range(args.steps):
+
+    # ablation: the copied-gradient path (dW to a private buffer, then a copy
+    # into the view) against direct placement, same steps, same replay mode
+    copied_ms = None
+    if not args.no_ablation:
+        c = StageBench(qe, torch, wl, use_graphs, dev, copy_gradients=True)
+        for _ in range(args.warmup):
+            c.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            c.step()
+        torch.cuda.synchronize()
+        copied_ms = (time.perf_counter() - t0) / args.steps * 1e3
+        c.ctx.close()
+        del c
+        torch.cuda.empty_cache()
+
+    # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
+    def instrumented(copy_gradients):
+        e = StageBench(qe, torch, wl, False, dev, copy_gradients=copy_gradients)
         e.step()
-    gemm_ms, gemm_n = e.ctx.qe_get_kernel_timing(qe.KC_GEMM)
-    q_ms, q_n = e.ctx.qe_get_kernel_timing(qe.KC_QUANT)
-    u_ms, u_n = e.ctx.qe_get_kernel_timing(qe.KC_UPDATE)
-    e.ctx.close()
+        torch.cuda.synchronize()
+        e.ctx.qe_set_kernel_timing(True)
+        for _ in range(args.steps):
+            e.step()
+        t = {k: e.ctx.qe_get_kernel_timing(k) for k in (qe.KC_GEMM, qe.KC_QUANT, qe.KC_UPDATE, qe.KC_COPY)}
+        e.ctx.close()
+        del e
+        torch.cuda.empty_cache()
+        return t
+
+    kt = instrumented(False)
+    gemm_ms, gemm_n = kt[qe.KC_GEMM]
+    q_ms, q_n = kt[qe.KC_QUANT]
+    u_ms, u_n = kt[qe.KC_UPDATE]
+    assert kt[qe.KC_COPY][1] == 0, "direct placement launched a gradient copy"
+    if copied_ms is not None:
+        c_ms, c_n = instrumented(True)[qe.KC_COPY]
+        # INIT placement (one microbatch): the copy reads the private FP32 dW and writes the view
+        copy_bytes = sum(8 * lin.n_out * lin.k_in for lin in wl.linears)
+        copy_gbs = copy_bytes * args.steps / (c_ms * 1e-3) / 1e9
     gemm_tflops = flops * args.steps / (gemm_ms * 1e-3) / 1e12
     qbytes = algorithmic_bytes(wl)
     q_gbs = qbytes * args.steps / (q_ms * 1e-3) / 1e9
@@ -242,7 +275,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4),
                      "traffic": gemm_traffic_per_launch(),
-                     "kernel": "gemm_tn_kernel (fwd + dI + dW launches)",
+                     "kernel": "gemm_tn_w4_kernel / gemm_tn_kernel (fwd + dI + dW launches)",
                      "avg_launch_us": round(gemm_ms / gemm_n * 1e3, 2), "launches": gemm_n},
         "quantize": {"achieved": round(q_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
                      "frac": round(q_gbs / HBM_PEAK_GBS, 4), "avg_launch_us": round(q_ms / q_n * 1e3, 2),
@@ -251,6 +284,12 @@ def main():
         "graph": {"captures": st["captures"], "replays": st["replays"], "handoffs": st["handoffs"],
                   "capture_ms": round(st["capture_ns"] / 1e6, 2)},
     }
+    if copied_ms is not None:
+        out["direct_placement_ablation"] = {
+            "copied_ms_per_step": round(copied_ms, 4), "direct_speedup_over_copied": round(copied_ms / ms, 4),
+            "copies_per_step_direct": 0, "copies_per_step_copied": c_n // args.steps,
+            "copy_bytes_per_step": copy_bytes, "copy_avg_launch_us": round(c_ms / c_n * 1e3, 2),
+            "copy_achieved_gbs": round(copy_gbs, 1), "copy_frac_hbm": round(copy_gbs / HBM_PEAK_GBS, 4)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
     print(json.dumps(out), flush=True)

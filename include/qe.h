@@ -151,7 +151,9 @@ typedef struct {
   int32_t use_graphs;    /* 1: capture each (layer, action, slot) sequence once and replay it */
   int32_t null_executor; /* 1: run the contract only, no HIP call at all (host-only testing) */
   int32_t one_way_handoff; /* testing only: skip the caller's wait on the graph tail (§2.3) */
-  int32_t reserved[3];
+  int32_t copy_gradients;  /* 1: dW goes to a private FP32 buffer, then is copied into the bound view
+                              (the copied-gradient path of §3.4, an ablation baseline); 0: direct */
+  int32_t reserved[2];
 } qe_config;
 
 typedef struct {
@@ -216,7 +218,9 @@ qe_status qe_fp8_linear_dgrad(qe_ctx *ctx, int32_t layer, qe_tape_key key, qe_ta
  * Device work: main_grad[offset + n*ld + k] (=, or +=)
  *   scale_inv(dY)_slot * scale_inv(X)_slot * sum_t dY_q^T[n][t] X_q^T[k][t]
  * using the snapshots kept in the slot, never the live scales; no FP8 state
- * update, no token advance.  Marks dW done and the view written; the slot is
+ * update, no token advance.  With qe_config.copy_gradients the GEMM writes a
+ * private [N, K] FP32 buffer and a second kernel copies (or adds) it into
+ * the view; the bits are the same as with direct placement.  Marks dW done and the view written; the slot is
  * released (payload dropped, generation kept) once dI and dW have both run. */
 qe_status qe_fp8_linear_wgrad_place(qe_ctx *ctx, int32_t layer, qe_tape_key key, qe_tape_ref ref,
                                     float *main_grad, int64_t offset, int64_t ld, qe_place_mode mode,
@@ -301,7 +305,8 @@ qe_status qe_inject_fault(qe_ctx *ctx, int32_t n);
 
 /* Kernel timing: when enabled (eager mode only), every kernel the context
  * launches is bracketed by HIP events on the graph stream; totals per kernel
- * class (0 quantize, 1 scale update, 2 GEMM) are read after a qe_sync. */
+ * class (0 quantize, 1 scale update, 2 GEMM, 3 gradient copy) are read after
+ * a qe_sync. */
 qe_status qe_set_kernel_timing(qe_ctx *ctx, int32_t enable);
 qe_status qe_get_kernel_timing(qe_ctx *ctx, int32_t kernel_class, double *total_ms_host, int64_t *launches_host);
 

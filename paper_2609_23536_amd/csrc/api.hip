@@ -33,6 +33,7 @@ struct Call {
     qe::QuantParams q;
     qe::UpdateParams u;
     qe::GemmParams g;
+    qe::GradCopyParams c;
   };
   Call() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
 };
@@ -55,6 +56,7 @@ struct LayerDev {
   uint8_t *w_q = nullptr, *w_q_t = nullptr;
   float *w_sinv = nullptr;
   uint8_t *x_q = nullptr, *dy_q = nullptr;  // row-wise scratch
+  float *grad_stage = nullptr;              // [N, K] FP32, copied-gradient path only
   int64_t ld_wq = 0, ld_wqt = 0, ld_xq = 0, ld_dyq = 0, ld_t = 0;
   std::vector<SlotDev> slots;
   std::vector<void *> allocs;
@@ -96,8 +98,8 @@ struct qe_ctx {
   int timing = 0;
   std::vector<TimedCall> timed;
   std::vector<hipEvent_t> event_pool;
-  double kc_ms[qe::KC_COUNT] = {0, 0, 0};
-  int64_t kc_n[qe::KC_COUNT] = {0, 0, 0};
+  double kc_ms[qe::KC_COUNT] = {0, 0, 0, 0};
+  int64_t kc_n[qe::KC_COUNT] = {0, 0, 0, 0};
   explicit qe_ctx(const qe_config &c) : cfg(c), contract(c.microbatches) {}
 };
 
@@ -110,6 +112,7 @@ hipError_t launch(const Call &c, hipStream_t s) {
   switch (c.kind) {
     case qe::KC_QUANT: return qe::launch_quantize(c.q, s);
     case qe::KC_UPDATE: return qe::launch_scale_update(c.u, s);
+    case qe::KC_COPY: return qe::launch_grad_copy(c.c, s);
     default: return qe::launch_gemm(c.g, s);
   }
 }
@@ -278,8 +281,23 @@ void append_wgrad(Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, float 
                   int mode) {
   const qe_layer_desc &d = L.desc;
   const SlotDev &S = L.slots[m];
+  if (L.grad_stage == nullptr) {  // direct placement: the GEMM epilogue writes the view
+    p.push_back(gemm_call(S.dy_q_t, d.fmt_dy, L.ld_t, S.x_q_t, d.fmt_x, L.ld_t, d.n_out, d.k_in, tokens, S.dy_sinv,
+                          S.x_sinv, mg + offset, QE_F32, ld, mode));
+    return;
+  }
+  // copied gradients: GEMM into the private buffer, then copy / add into the view
   p.push_back(gemm_call(S.dy_q_t, d.fmt_dy, L.ld_t, S.x_q_t, d.fmt_x, L.ld_t, d.n_out, d.k_in, tokens, S.dy_sinv,
-                        S.x_sinv, mg + offset, QE_F32, ld, mode));
+                        S.x_sinv, L.grad_stage, QE_F32, d.k_in, QE_PLACE_INIT));
+  Call c;
+  c.kind = qe::KC_COPY;
+  c.c.src = L.grad_stage;
+  c.c.dst = mg + offset;
+  c.c.n = d.n_out;
+  c.c.k = d.k_in;
+  c.c.ld = ld;
+  c.c.accumulate = mode == QE_PLACE_ACCUM;
+  p.push_back(c);
 }
 
 qe_status fail_physical(qe_ctx *c) {
@@ -468,6 +486,8 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
     L.w_sinv = static_cast<float *>(dev_alloc(c, L, sizeof(float), &ok));
     L.x_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->max_tokens) * L.ld_xq, &ok));
     L.dy_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->max_tokens) * L.ld_dyq, &ok));
+    if (c->cfg.copy_gradients)
+      L.grad_stage = static_cast<float *>(dev_alloc(c, L, sizeof(float) * size_t(d->n_out) * size_t(d->k_in), &ok));
     for (auto &S : L.slots) {
       S.x_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->k_in) * L.ld_t, &ok));
       S.dy_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->n_out) * L.ld_t, &ok));

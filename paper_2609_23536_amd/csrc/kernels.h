@@ -58,10 +58,20 @@ struct GemmParams {
   int32_t pad;
 };
 
-enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COUNT = 3 };
+// dst[n * ld + k] (=, or +=) src[n * k + k'] for the copied-gradient path.
+struct GradCopyParams {
+  const float *src;  // [n, k] dense
+  float *dst;        // [n, ld] view
+  int64_t n, k, ld;
+  int32_t accumulate;
+  int32_t pad;
+};
+
+enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COPY = 3, KC_COUNT = 4 };
 
 hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s);
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
+hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s);
 
 }  // namespace qe

@@ -19,7 +19,7 @@ E4M3, E5M2 = 0, 1
 F32, BF16 = 0, 1
 INIT, ACCUM = 0, 1
 ROLE_X, ROLE_W, ROLE_DY = 0, 1, 2
-KC_QUANT, KC_UPDATE, KC_GEMM = 0, 1, 2
+KC_QUANT, KC_UPDATE, KC_GEMM, KC_COPY = 0, 1, 2, 3
 
 STATUS = ["OK", "INVALID_ARG", "STALE_REF", "KEY_MISMATCH", "KEY_LIVE", "POOL_FULL", "DUPLICATE_CONSUMER", "ORDER",
           "EPOCH", "STALE_CACHE", "DEST_MISMATCH", "DEST_ALIAS", "DUP_WRITE", "ARENA_INVALID", "INCOMPLETE",
@@ -48,7 +48,8 @@ class FP8Meta(C.Structure):
 
 class Config(C.Structure):
     _fields_ = [("device", C.c_int32), ("microbatches", C.c_int32), ("use_graphs", C.c_int32),
-                ("null_executor", C.c_int32), ("one_way_handoff", C.c_int32), ("reserved", C.c_int32 * 3)]
+                ("null_executor", C.c_int32), ("one_way_handoff", C.c_int32), ("copy_gradients", C.c_int32),
+                ("reserved", C.c_int32 * 2)]
 
 
 class LayerDesc(C.Structure):
@@ -185,8 +186,9 @@ class Context:
     """Owns one qe_ctx.  Methods forward to the C calls of the same name."""
 
     def __init__(self, microbatches: int, use_graphs: bool = False, null_executor: bool = False, device: int = 0,
-                 one_way_handoff: bool = False):
-        cfg = Config(device, microbatches, int(use_graphs), int(null_executor), int(one_way_handoff))
+                 one_way_handoff: bool = False, copy_gradients: bool = False):
+        cfg = Config(device, microbatches, int(use_graphs), int(null_executor), int(one_way_handoff),
+                     int(copy_gradients))
         h = C.c_void_p()
         st = _st(lib().qe_ctx_create(C.byref(cfg), C.byref(h)))
         if st != "OK":

@@ -44,10 +44,10 @@ class Spec:
 
 
 class GpuStage:
-    def __init__(self, qe, spec, use_graphs=False, device=None):
+    def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False):
         self.qe, self.spec = qe, spec
         self.d = device
-        self.ctx = qe.Context(spec.M, use_graphs=use_graphs)
+        self.ctx = qe.Context(spec.M, use_graphs=use_graphs, copy_gradients=copy_gradients)
         dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
         self.w = [upload(spec.weight(u), self.d) for u in range(len(spec.shapes))]
         for u, (n, k) in enumerate(spec.shapes):

@@ -125,9 +125,9 @@ def test_empty_microbatch():
     assert np.all(g.grad.cpu().numpy() == 0)
 
 
-def _run_variant(spec, steps, use_graphs, full):
+def _run_variant(spec, steps, use_graphs, full, copy_gradients=False):
     qe = need_lib()
-    g = GpuStage(qe, spec, use_graphs=use_graphs, device=dev())
+    g = GpuStage(qe, spec, use_graphs=use_graphs, device=dev(), copy_gradients=copy_gradients)
     o = OracleStage(spec)
     grads = []
     for step, sched in enumerate(steps):
@@ -181,3 +181,20 @@ def test_graph_replay_bitwise_equals_eager():
     # when pointers change; every action still went through a graph launch
     assert st["replays"] == sum(len(s) for s in steps) * 2
     assert st["graphs"] > 0 and st["handoffs"] == 2 * st["replays"]
+
+
+@pytest.mark.parametrize("case", ["single", "zb"])
+@pytest.mark.parametrize("use_graphs", [False, True])
+def test_copied_gradients_bitwise_equal_direct_placement(case, use_graphs):
+    """The copied-gradient path (dW into a private buffer, then a copy / add into
+    the view) gives the same bits as direct placement, shared views included."""
+    if case == "single":
+        spec = Spec([(256, 256)], tokens=128, M=2, history=4, margin=0, in_dtype="f32", shared_view=True, cfg=0)
+        steps = [S.SINGLE, S.SINGLE]
+    else:
+        spec = Spec([(96, 160), (72, 200)], tokens=48, M=8, history=16, margin=0, in_dtype="bf16",
+                    shared_view=False, cfg=2)
+        steps = [S.ZB_STEP0, S.ZB_STEP1]
+    direct = _run_variant(spec, steps, use_graphs, False)
+    copied = _run_variant(spec, steps, use_graphs, False, copy_gradients=True)
+    _assert_bitwise(direct, copied)
