@@ -17,6 +17,10 @@ dW(m): dW_m = dY_q^T X_q using the two scale_inv values kept in slot m, never
 The W role is updated with every forward but records an amax only when the
 cache is refreshed (§2.1: the quantized weight is cached across microbatches
 and refreshed only in the first forward after an optimizer step).
+
+A layer with current (dynamic) scaling runs the same actions, but each tensor
+is cast with a scale set from its own amax just before the cast (X in F, W on
+a cache refresh, dY in dI); there is no history and nothing is recorded.
 """
 from __future__ import annotations
 
@@ -27,7 +31,7 @@ import numpy as np
 
 from . import contract as C
 from .gemm import gemm_tn, place, quantize_with_amax
-from .scaling import DelayedScaler
+from .scaling import CurrentScaler, DelayedScaler
 
 
 @dataclasses.dataclass
@@ -40,12 +44,20 @@ class Payload:
 
 class OracleLayer:
     def __init__(self, w_f32: np.ndarray, history: int, margin: int, fmt_x: str, fmt_w: str, fmt_dy: str,
-                 microbatches: int):
+                 microbatches: int, scaling: str = "delayed"):
         self.w = np.asarray(w_f32, dtype=np.float32)
         self.fmt_x, self.fmt_w, self.fmt_dy = fmt_x, fmt_w, fmt_dy
-        self.sx = DelayedScaler(fmt_x, history, margin)
-        self.sw = DelayedScaler(fmt_w, history, margin)
-        self.sdy = DelayedScaler(fmt_dy, history, margin)
+        if scaling not in ("delayed", "current"):
+            raise ValueError(scaling)
+        self.current = scaling == "current"
+        if self.current:
+            self.sx = CurrentScaler(fmt_x, margin)
+            self.sw = CurrentScaler(fmt_w, margin)
+            self.sdy = CurrentScaler(fmt_dy, margin)
+        else:
+            self.sx = DelayedScaler(fmt_x, history, margin)
+            self.sw = DelayedScaler(fmt_w, history, margin)
+            self.sdy = DelayedScaler(fmt_dy, history, margin)
         self.wq = self.wq_t = None
         self.w_scale_inv = 1.0
         self.payload: List[Payload] = [Payload() for _ in range(microbatches)]
@@ -60,10 +72,10 @@ class Stage:
         self.arena: Dict[int, np.ndarray] = {}   # buffer address -> float32 flat buffer
 
     def add_layer(self, stage: int, unit: int, w_f32: np.ndarray, max_tokens: int, history: int, margin: int,
-                  fmt_x: str = "E4M3", fmt_w: str = "E4M3", fmt_dy: str = "E5M2") -> int:
+                  fmt_x: str = "E4M3", fmt_w: str = "E4M3", fmt_dy: str = "E5M2", scaling: str = "delayed") -> int:
         n, k = w_f32.shape
         idx = self.contract.add_layer(stage, unit, n, k, max_tokens)
-        self.layers.append(OracleLayer(w_f32, history, margin, fmt_x, fmt_w, fmt_dy, self.contract.M))
+        self.layers.append(OracleLayer(w_f32, history, margin, fmt_x, fmt_w, fmt_dy, self.contract.M, scaling))
         return idx
 
     def set_weight(self, layer: int, w_f32: np.ndarray) -> None:
@@ -86,6 +98,18 @@ class Stage:
             self.contract.abort()
             return C.EXEC_FAILED, None, None
         L = self.layers[layer]
+        if L.current:
+            if refresh:
+                L.sw.set_from(L.w)
+                L.wq, L.wq_t, _ = quantize_with_amax(L.w, L.sw.scale, L.fmt_w)
+                L.w_scale_inv = L.sw.scale_inv
+            L.sx.set_from(x_f32)
+            xq, xq_t, _ = quantize_with_amax(x_f32, L.sx.scale, L.fmt_x)
+            P = L.payload[key[2]]
+            P.xq_t, P.x_scale_inv = xq_t, L.sx.scale_inv
+            y = gemm_tn(xq, L.fmt_x, L.wq, L.fmt_w, P.x_scale_inv, L.w_scale_inv)
+            ref = self.contract.commit_fwd(layer, key, tokens, refresh)
+            return C.OK, y, ref
         if refresh:
             L.wq, L.wq_t, a_w = quantize_with_amax(L.w, L.sw.scale, L.fmt_w)
             L.w_scale_inv = L.sw.scale_inv
@@ -104,11 +128,14 @@ class Stage:
     def _dgrad_physical(self, layer: int, ref, dy_f32: np.ndarray):
         L = self.layers[layer]
         P = L.payload[ref[0]]
+        if L.current:
+            L.sdy.set_from(dy_f32)
         dyq, dyq_t, a_dy = quantize_with_amax(dy_f32, L.sdy.scale, L.fmt_dy)
         P.dyq_t, P.dy_scale_inv = dyq_t, L.sdy.scale_inv
-        L.sdy.record(a_dy)
         dx = gemm_tn(dyq, L.fmt_dy, L.wq_t, L.fmt_w, P.dy_scale_inv, L.w_scale_inv)
-        L.sdy.update()
+        if not L.current:
+            L.sdy.record(a_dy)
+            L.sdy.update()
         return dx
 
     def dgrad(self, layer: int, key, ref, dy_f32: np.ndarray):
@@ -178,4 +205,6 @@ class Stage:
 
     def fp8_state(self, layer: int) -> dict:
         L = self.layers[layer]
+        if L.current:   # no history: a one-entry history that is always clear
+            return {r: (np.zeros(1), s.scale, s.scale_inv) for r, s in (("x", L.sx), ("w", L.sw), ("dy", L.sdy))}
         return {r: (s.hist.copy(), s.scale, s.scale_inv) for r, s in (("x", L.sx), ("w", L.sw), ("dy", L.sdy))}

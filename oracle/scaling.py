@@ -18,6 +18,15 @@ the readings taken here are:
   the last slot) and slot 0 is cleared, so the update after the k-th record
   sees the last H recorded amaxes.
 * Initial state: history all zero, scale = scale_inv = 1.
+
+Current (dynamic) scaling, which §2.1 names beside delayed scaling as a
+target and which §4.2 allows at the last stage's output boundary, inspects
+the operand itself: its scale comes from the amax of the tensor about to be
+cast.
+The paper prints no formula for it either; the reading taken here keeps the
+delayed rule's exponent and its degenerate case, applied to that one amax:
+e = floor(log2(fmax / max|x|)) - margin (clamped as above), and a tensor whose
+amax is 0, inf or NaN keeps the role's previous scale.  No history is kept.
 """
 from __future__ import annotations
 
@@ -83,3 +92,20 @@ class DelayedScaler:
         s.hist = self.hist.copy()
         s.scale, s.scale_inv = self.scale, self.scale_inv
         return s
+
+
+class CurrentScaler:
+    """Scale of one tensor role under current (dynamic) scaling: no history;
+    the scale is set from the amax of the tensor it is about to cast."""
+
+    def __init__(self, fmt, margin: int):
+        self.fmt = fmt_of(fmt)
+        self.margin = int(margin)
+        self.scale = 1.0
+        self.scale_inv = 1.0
+
+    def set_from(self, x) -> None:
+        e = scale_exponent(amax(x), self.fmt, self.margin)
+        if e is not None:
+            self.scale = math.ldexp(1.0, e)
+            self.scale_inv = math.ldexp(1.0, -e)
