@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the copied-gradient passes (direct placement only)")
+    ap.add_argument("--no-current", action="store_true", help="skip the current-scaling passes")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
@@ -81,7 +82,7 @@ def copy_calibration(nbytes):
 
 
 class StageBench:
-    def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False):
+    def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False, current=False):
         import workloads as W
         self.qe, self.torch, self.wl, self.d = qe, torch, wl, device
         self.ctx = qe.Context(1, use_graphs=use_graphs, copy_gradients=copy_gradients)
@@ -104,7 +105,8 @@ class StageBench:
             self.y.append(torch.empty((wl.tokens, lin.n_out), dtype=tdt, device=device))
             self.dx.append(torch.empty((wl.tokens, lin.k_in), dtype=tdt, device=device))
             st, idx = self.ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, wl.tokens, self.w[u], self.dt,
-                                                 wl.history, wl.margin)
+                                                 1 if current else wl.history, wl.margin,
+                                                 scaling=qe.SCALING_CURRENT if current else qe.SCALING_DELAYED)
             assert st == "OK" and idx == u, st
         self.grad = torch.zeros(wl.flat_grad_elems(), dtype=torch.float32, device=device)
         self.offs = wl.grad_offsets()
@@ -132,7 +134,25 @@ class StageBench:
         self.epoch += 1
 
 
-def algorithmic_bytes(wl):
+def timed_ms(b, torch, warmup, steps):
+    """Mean wall time of `steps` steps after `warmup` untimed ones, device-synchronised."""
+    for _ in range(warmup):
+        b.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        b.step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps * 1e3
+
+
+def amax_bytes(wl):
+    """Per step under current scaling: the amax pass reads X, dY and (refresh) W once each."""
+    b_in = 2 if wl.in_dtype == "bf16" else 4
+    return sum((wl.tokens * (lin.k_in + lin.n_out) + lin.n_out * lin.k_in) * b_in for lin in wl.linears)
+
+
+def qbytes_per_step(wl):
     """Per step: quantize bytes (in + row codes + column codes) of X, dY and the W refresh."""
     b_in = 2 if wl.in_dtype == "bf16" else 4
     q = 0
@@ -224,27 +244,33 @@ def main():
     copied_ms = None
     if not args.no_ablation:
         c = StageBench(qe, torch, wl, use_graphs, dev, copy_gradients=True)
-        for _ in range(args.warmup):
-            c.step()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            c.step()
-        torch.cuda.synchronize()
-        copied_ms = (time.perf_counter() - t0) / args.steps * 1e3
+        copied_ms = timed_ms(c, torch, args.warmup, args.steps)
+        c.ctx.close()
+        del c
+        torch.cuda.empty_cache()
+
+    # current (dynamic) scaling: the same step with every cast scaled by its own tensor's amax
+    current_ms = None
+    if not args.no_current:
+        c = StageBench(qe, torch, wl, use_graphs, dev, current=True)
+        current_ms = timed_ms(c, torch, args.warmup, args.steps)
+        assert c.ctx.qe_sync() == "OK"
+        cst = c.ctx.qe_get_state()
+        assert cst["device_token"] == cst["token"]
         c.ctx.close()
         del c
         torch.cuda.empty_cache()
 
     # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
-    def instrumented(copy_gradients):
-        e = StageBench(qe, torch, wl, False, dev, copy_gradients=copy_gradients)
+    def instrumented(copy_gradients=False, current=False):
+        e = StageBench(qe, torch, wl, False, dev, copy_gradients=copy_gradients, current=current)
         e.step()
         torch.cuda.synchronize()
         e.ctx.qe_set_kernel_timing(True)
         for _ in range(args.steps):
             e.step()
-        t = {k: e.ctx.qe_get_kernel_timing(k) for k in (qe.KC_GEMM, qe.KC_QUANT, qe.KC_UPDATE, qe.KC_COPY)}
+        t = {k: e.ctx.qe_get_kernel_timing(k)
+             for k in (qe.KC_GEMM, qe.KC_QUANT, qe.KC_UPDATE, qe.KC_COPY, qe.KC_AMAX)}
         e.ctx.close()
         del e
         torch.cuda.empty_cache()
@@ -256,12 +282,18 @@ def main():
     u_ms, u_n = kt[qe.KC_UPDATE]
     assert kt[qe.KC_COPY][1] == 0, "direct placement launched a gradient copy"
     if copied_ms is not None:
-        c_ms, c_n = instrumented(True)[qe.KC_COPY]
+        c_ms, c_n = instrumented(copy_gradients=True)[qe.KC_COPY]
         # INIT placement (one microbatch): the copy reads the private FP32 dW and writes the view
         copy_bytes = sum(8 * lin.n_out * lin.k_in for lin in wl.linears)
         copy_gbs = copy_bytes * args.steps / (c_ms * 1e-3) / 1e9
+    if current_ms is not None:
+        kc = instrumented(current=True)
+        a_ms, a_n = kc[qe.KC_AMAX]
+        cq_ms, cq_n = kc[qe.KC_QUANT]
+        a_gbs = amax_bytes(wl) * args.steps / (a_ms * 1e-3) / 1e9
+        cq_gbs = qbytes_per_step(wl) * args.steps / (cq_ms * 1e-3) / 1e9
     gemm_tflops = flops * args.steps / (gemm_ms * 1e-3) / 1e12
-    qbytes = algorithmic_bytes(wl)
+    qbytes = qbytes_per_step(wl)
     q_gbs = qbytes * args.steps / (q_ms * 1e-3) / 1e9
 
     out = {
@@ -290,6 +322,15 @@ def main():
             "copies_per_step_direct": 0, "copies_per_step_copied": c_n // args.steps,
             "copy_bytes_per_step": copy_bytes, "copy_avg_launch_us": round(c_ms / c_n * 1e3, 2),
             "copy_achieved_gbs": round(copy_gbs, 1), "copy_frac_hbm": round(copy_gbs / HBM_PEAK_GBS, 4)}
+    if current_ms is not None:
+        out["current_scaling"] = {
+            "ms_per_step": round(current_ms, 4), "value": round(flops / (current_ms * 1e-3) / 1e12, 2),
+            "unit": "TFLOP/s", "step_time_vs_delayed": round(current_ms / ms, 4),
+            "amax": {"achieved": round(a_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                     "frac": round(a_gbs / HBM_PEAK_GBS, 4), "avg_launch_us": round(a_ms / a_n * 1e3, 2),
+                     "launches": a_n, "bytes_per_step": amax_bytes(wl)},
+            "quantize": {"achieved": round(cq_gbs, 1), "unit": "GB/s", "frac": round(cq_gbs / HBM_PEAK_GBS, 4),
+                         "avg_launch_us": round(cq_ms / cq_n * 1e3, 2), "launches": cq_n}}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
     print(json.dumps(out), flush=True)

@@ -67,6 +67,10 @@ typedef enum { QE_E4M3 = 0, QE_E5M2 = 1 } qe_fp8_fmt;   /* OCP FP8 formats (max 
 typedef enum { QE_F32 = 0, QE_BF16 = 1 } qe_dtype;
 typedef enum { QE_PLACE_INIT = 0, QE_PLACE_ACCUM = 1 } qe_place_mode;
 typedef enum { QE_ROLE_X = 0, QE_ROLE_W = 1, QE_ROLE_DY = 2 } qe_role;
+/* Scaling recipe of a layer: delayed (scales from the amax history, §2.1) or
+ * current / dynamic (each tensor's scale from its own amax, the kind of
+ * output boundary §4.2 allows at the last stage). */
+typedef enum { QE_SCALING_DELAYED = 0, QE_SCALING_CURRENT = 1 } qe_scaling;
 
 /* TapeKey K = (e, s, m, u, i): optimizer epoch, pipeline stage, microbatch,
  * sub-layer unit, invocation counter (§3.1). */
@@ -79,9 +83,21 @@ typedef struct {
   uint32_t slot, generation;
 } qe_tape_ref;
 
+/* Amax accumulator: QE_AMAX_LINES floats spaced QE_AMAX_STRIDE floats
+ * (256 bytes) apart, QE_AMAX_LINES * QE_AMAX_STRIDE floats (16 KiB) in all,
+ * zero-initialised.  Its value is the max over the lines.  Producers fold a
+ * workgroup's max into line (workgroup % QE_AMAX_LINES), so concurrent
+ * workgroups never contend for one cache line: device-scope atomics on one
+ * line serialise at the memory side (about 11 ns each on MI355X), which a
+ * single accumulator float would pay once per workgroup. */
+#define QE_AMAX_LINES 64
+#define QE_AMAX_STRIDE 64
+
 /* Delayed-scaling state of one tensor role (§2.1): all device pointers.
- * amax_history[history_len]; scale and scale_inv are single floats.
- * Initial state: history all zero, scale = scale_inv = 1. */
+ * amax_history[history_len]; scale and scale_inv are single floats;
+ * amax_accum is an optional amax accumulator (NULL: amaxes are folded into
+ * amax_history[0] directly).  Initial state: history and accumulator all
+ * zero, scale = scale_inv = 1. */
 typedef struct {
   float *amax_history;
   float *scale;
@@ -90,6 +106,7 @@ typedef struct {
   int32_t margin;
   int32_t fmt; /* qe_fp8_fmt */
   int32_t reserved;
+  float *amax_accum;
 } qe_fp8_meta;
 
 /* ------------------------------------------------------------------------
@@ -97,7 +114,9 @@ typedef struct {
  * ------------------------------------------------------------------------ */
 
 /* Delayed scale update (§2.1; the S0->S1 / S1->S2 transitions of §3.2) for
- * n_metas roles in one launch.  For each meta: a = max(amax_history[0..H-1])
+ * n_metas roles in one launch.  For each meta: if amax_accum is set, its
+ * value is first folded into amax_history[0] (max) and its lines cleared;
+ * then a = max(amax_history[0..H-1])
  * (NaN propagates); if a is finite and > 0, e = floor(log2(fmax/a)) - margin
  * clamped to [-126, 126], scale = 2^e, scale_inv = 2^-e, else scale is kept;
  * then the history rotates one place towards index 0 (index 0 moves to H-1)
@@ -113,14 +132,38 @@ qe_status qe_amax_scale_update(const qe_fp8_meta *metas_host, int32_t n_metas, i
  * Writes q_row[r * ld_row + c] = Q(in[r][c] * scale) and
  *        q_col[c * ld_col + r] = the same code (the transpose),
  * where Q rounds to nearest even and saturates to +-fmax (NaN -> 0x7F|sign).
- * Either output may be NULL.  max|in| (unscaled) is folded into
- * meta->amax_history[0] with a max (NaN propagates).  If scale_inv_snapshot
+ * Either output may be NULL.  max|in| (unscaled) is folded with a max (NaN
+ * propagates) into meta->amax_accum if set (it then reaches amax_history[0]
+ * at the next qe_amax_scale_update), else into meta->amax_history[0].  If scale_inv_snapshot
  * is non-null the scale_inv paired with the scale used is copied there.
  * Layout rules: ld_row >= cols, ld_col >= rows.  rows or cols may be 0.
  * Errors: QE_ERR_INVALID_ARG; QE_ERR_HIP. */
 qe_status qe_quantize_fp8(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols, const qe_fp8_meta *meta_host,
                           uint8_t *q_row, int64_t ld_row, uint8_t *q_col, int64_t ld_col, float *scale_inv_snapshot,
                           qe_stream stream);
+
+/* Amax of a tensor (§2.1): max |in[i]| over the numel contiguous elements of
+ * in (QE_F32 or QE_BF16), computed exactly, folded with a max (NaN
+ * propagates) into the role's amax slot: meta->amax_accum if set, else
+ * meta->amax_history[0].  numel may be 0.  in must be aligned to its element
+ * size.  Errors: QE_ERR_INVALID_ARG; QE_ERR_HIP. */
+qe_status qe_amax(const void *in, qe_dtype in_dtype, int64_t numel, const qe_fp8_meta *meta_host, qe_stream stream);
+
+/* Current (dynamic) scaling cast: the scale is set from the amax of `in`
+ * itself, then `in` is cast with it (the dynamic alternative to delayed
+ * scaling, §2.1; a last-stage boundary in §4.2).  Three launches on `stream`:
+ * qe_amax into the role's amax slot, the scale update of
+ * qe_amax_scale_update (so e = floor(log2(fmax / amax)) - margin, an amax of
+ * 0, inf or NaN keeps the previous scale, and the slot is cleared again),
+ * then the cast of qe_quantize_fp8 without recording an amax.  The meta must
+ * have history_len == 1 and a clear amax slot on entry (as initialised and
+ * as every call leaves it).  Other arguments as for qe_quantize_fp8;
+ * device_token as for qe_amax_scale_update.
+ * Errors: QE_ERR_INVALID_ARG (also for history_len != 1); QE_ERR_HIP. */
+qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols,
+                                  const qe_fp8_meta *meta_host, uint8_t *q_row, int64_t ld_row, uint8_t *q_col,
+                                  int64_t ld_col, float *scale_inv_snapshot, int64_t *device_token,
+                                  qe_stream stream);
 
 /* FP8 GEMM in "TN" form (both operands contiguous along the reduction axis):
  *     D[i][j] = (a_scale_inv * b_scale_inv) * sum_r A[i][r] * B[j][r]
@@ -165,7 +208,7 @@ typedef struct {
   int32_t history_len;   /* amax history length H (all roles) */
   int32_t margin;        /* scale margin (all roles) */
   int32_t fmt_x, fmt_w, fmt_dy; /* qe_fp8_fmt per role */
-  int32_t reserved;
+  int32_t scaling;       /* qe_scaling; QE_SCALING_CURRENT requires history_len == 1 */
 } qe_layer_desc;
 
 /* Create a context.  Allocates the graph stream and events (unless
@@ -176,7 +219,10 @@ void qe_ctx_destroy(qe_ctx *ctx);
 /* Register a linear layer.  Allocates its FP8 state (three roles), its
  * quantized-weight cache W_q [N,K] and W_q^T [K,N], one tape payload per slot
  * (X_q^T [K, tokens], dY_q^T [N, tokens] and the two scale_inv snapshots),
- * and scratch for the row-wise X_q / dY_q.  (stage, unit) must be unique. */
+ * and scratch for the row-wise X_q / dY_q.  (stage, unit) must be unique.
+ * With desc->scaling == QE_SCALING_CURRENT every cast below takes its scale
+ * from the amax of the tensor it casts (qe_quantize_fp8_current's sequence)
+ * instead of from the history; nothing else about the actions changes. */
 qe_status qe_layer_register(qe_ctx *ctx, const qe_layer_desc *desc_host, int32_t *layer_out_host);
 
 /* Device pointers of a role's FP8 state (for inspection / checkpointing). */
@@ -197,6 +243,8 @@ qe_status qe_layer_slot_payload(const qe_ctx *ctx, int32_t layer, int32_t slot, 
  * scratch), record amax(X), snapshot scale_inv(X); Y = X W^T in FP8; update
  * the X and W scales.  Then the slot's generation is advanced, the key bound
  * and the effect token advanced; *ref_out_host receives (slot, generation).
+ * Current scaling: amax(X) [and amax(W) on refresh] first, then the X [and
+ * W] scale update, then the casts without recording, then the GEMM.
  * x: [tokens, K] (QE_F32/QE_BF16); y: [tokens, N] (QE_F32/QE_BF16). */
 qe_status qe_fp8_linear_fwd(qe_ctx *ctx, int32_t layer, qe_tape_key key, const void *x, qe_dtype x_dtype,
                             int64_t tokens, void *y, qe_dtype y_dtype, qe_tape_ref *ref_out_host,
@@ -206,7 +254,8 @@ qe_status qe_fp8_linear_fwd(qe_ctx *ctx, int32_t layer, qe_tape_key key, const v
  * require dI not yet run.  Device work: quantize dY once (the slot's dY_q^T +
  * row-wise scratch), record amax(dY), snapshot scale_inv(dY); dX = dY W in
  * FP8 using the cached W_q^T; update the dY scale.  Marks dI done, advances the
- * effect token.  dy: [tokens, N]; dx: [tokens, K]. */
+ * effect token.  Current scaling: amax(dY), the dY scale update, then the
+ * cast without recording, then the GEMM.  dy: [tokens, N]; dx: [tokens, K]. */
 qe_status qe_fp8_linear_dgrad(qe_ctx *ctx, int32_t layer, qe_tape_key key, qe_tape_ref ref, const void *dy,
                               qe_dtype dy_dtype, void *dx, qe_dtype dx_dtype, qe_stream caller);
 

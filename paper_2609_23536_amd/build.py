@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libqe.so")
 
-HIP_SOURCES = ["api.hip", "quantize.hip", "scale_update.hip", "gemm_fp8.hip", "grad_copy.hip"]
+HIP_SOURCES = ["api.hip", "quantize.hip", "scale_update.hip", "gemm_fp8.hip", "grad_copy.hip", "amax.hip"]
 CXX_SOURCES = ["contract.cpp"]
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",

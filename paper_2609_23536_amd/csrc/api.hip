@@ -34,6 +34,7 @@ struct Call {
     qe::UpdateParams u;
     qe::GemmParams g;
     qe::GradCopyParams c;
+    qe::AmaxParams a;
   };
   Call() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
 };
@@ -52,7 +53,8 @@ struct SlotDev {
 
 struct LayerDev {
   qe_layer_desc desc{};
-  float *meta = nullptr;  // hist[3][H] | scale[3] | scale_inv[3]
+  float *meta = nullptr;   // hist[3][H] | scale[3] | scale_inv[3]
+  float *accum = nullptr;  // amax accumulators of the three roles
   uint8_t *w_q = nullptr, *w_q_t = nullptr;
   float *w_sinv = nullptr;
   uint8_t *x_q = nullptr, *dy_q = nullptr;  // row-wise scratch
@@ -70,6 +72,7 @@ struct LayerDev {
     m.history_len = H;
     m.margin = desc.margin;
     m.fmt = r == QE_ROLE_X ? desc.fmt_x : (r == QE_ROLE_W ? desc.fmt_w : desc.fmt_dy);
+    m.accum = accum ? accum + size_t(r) * qe::kAmaxLines * qe::kAmaxStride : nullptr;
     return m;
   }
 };
@@ -98,8 +101,8 @@ struct qe_ctx {
   int timing = 0;
   std::vector<TimedCall> timed;
   std::vector<hipEvent_t> event_pool;
-  double kc_ms[qe::KC_COUNT] = {0, 0, 0, 0};
-  int64_t kc_n[qe::KC_COUNT] = {0, 0, 0, 0};
+  double kc_ms[qe::KC_COUNT] = {};
+  int64_t kc_n[qe::KC_COUNT] = {};
   explicit qe_ctx(const qe_config &c) : cfg(c), contract(c.microbatches) {}
 };
 
@@ -107,12 +110,14 @@ namespace {
 
 bool valid_dtype(int d) { return d == QE_F32 || d == QE_BF16; }
 bool valid_fmt(int f) { return f == QE_E4M3 || f == QE_E5M2; }
+bool elem_aligned(const void *p, int dt) { return uintptr_t(p) % (dt == QE_BF16 ? 2 : 4) == 0; }
 
 hipError_t launch(const Call &c, hipStream_t s) {
   switch (c.kind) {
     case qe::KC_QUANT: return qe::launch_quantize(c.q, s);
     case qe::KC_UPDATE: return qe::launch_scale_update(c.u, s);
     case qe::KC_COPY: return qe::launch_grad_copy(c.c, s);
+    case qe::KC_AMAX: return qe::launch_amax(c.a, s);
     default: return qe::launch_gemm(c.g, s);
   }
 }
@@ -200,7 +205,7 @@ uint64_t graph_key(int layer, int action, uint32_t slot) {
 enum { ACT_FWD = 1, ACT_FWD_REFRESH = 2, ACT_DGRAD = 3, ACT_WGRAD = 4, ACT_FULL = 5 };
 
 Call quant_call(const void *in, int in_dt, int64_t rows, int64_t cols, const qe::MetaRef &m, uint8_t *q_row,
-                int64_t ld_row, uint8_t *q_col, int64_t ld_col, float *snapshot) {
+                int64_t ld_row, uint8_t *q_col, int64_t ld_col, float *snapshot, bool record = true) {
   Call c;
   c.kind = qe::KC_QUANT;
   c.q.in = in;
@@ -210,7 +215,8 @@ Call quant_call(const void *in, int in_dt, int64_t rows, int64_t cols, const qe:
   c.q.cols = cols;
   c.q.scale = m.scale;
   c.q.scale_inv = m.scale_inv;
-  c.q.amax_slot = m.hist;
+  c.q.amax_slot = record ? m.hist : nullptr;
+  c.q.amax_accum = record ? m.accum : nullptr;
   c.q.q_row = q_row;
   c.q.ld_row = ld_row;
   c.q.q_col = q_col;
@@ -240,6 +246,13 @@ Call gemm_call(const uint8_t *a, int fa, int64_t lda, const uint8_t *b, int fb, 
   return c;
 }
 
+Call amax_call(const void *in, int in_dt, int64_t numel, const qe::MetaRef &m) {
+  Call c;
+  c.kind = qe::KC_AMAX;
+  c.a = qe::amax_params(in, in_dt == QE_BF16, numel, m.hist, m.accum);
+  return c;
+}
+
 Call update_call(const LayerDev &L, std::initializer_list<int> roles, long long *token) {
   Call c;
   c.kind = qe::KC_UPDATE;
@@ -256,6 +269,19 @@ Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt,
   const qe_layer_desc &d = L.desc;
   const SlotDev &S = L.slots[m];
   Plan p;
+  if (d.scaling == QE_SCALING_CURRENT) {  // amax first, then the scales, then the casts
+    if (refresh) p.push_back(amax_call(d.w, d.w_dtype, d.n_out * d.k_in, L.role(QE_ROLE_W)));
+    p.push_back(amax_call(x, x_dt, tokens * d.k_in, L.role(QE_ROLE_X)));
+    p.push_back(refresh ? update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token) : update_call(L, {QE_ROLE_X}, c->d_token));
+    if (refresh)
+      p.push_back(quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt,
+                             L.w_sinv, false));
+    p.push_back(
+        quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv, false));
+    p.push_back(gemm_call(L.x_q, d.fmt_x, L.ld_xq, L.w_q, d.fmt_w, L.ld_wq, tokens, d.n_out, d.k_in, S.x_sinv,
+                          L.w_sinv, y, y_dt, d.n_out, QE_PLACE_INIT));
+    return p;
+  }
   if (refresh)
     p.push_back(quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt,
                            L.w_sinv));
@@ -266,15 +292,25 @@ Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt,
   return p;
 }
 
+// dI's cast and GEMM.  Under delayed scaling the dY update is appended by the
+// caller after the action's last use of the old scale (finish_dgrad).
 void append_dgrad(qe_ctx *c, Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, const void *dy, int dy_dt,
                   void *dx, int dx_dt) {
-  (void)c;
   const qe_layer_desc &d = L.desc;
   const SlotDev &S = L.slots[m];
+  const bool current = d.scaling == QE_SCALING_CURRENT;
+  if (current) {
+    p.push_back(amax_call(dy, dy_dt, tokens * d.n_out, L.role(QE_ROLE_DY)));
+    p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+  }
   p.push_back(quant_call(dy, dy_dt, tokens, d.n_out, L.role(QE_ROLE_DY), L.dy_q, L.ld_dyq, S.dy_q_t, L.ld_t,
-                         S.dy_sinv));
+                         S.dy_sinv, !current));
   p.push_back(gemm_call(L.dy_q, d.fmt_dy, L.ld_dyq, L.w_q_t, d.fmt_w, L.ld_wqt, tokens, d.k_in, d.n_out, S.dy_sinv,
                         L.w_sinv, dx, dx_dt, d.k_in, QE_PLACE_INIT));
+}
+
+void finish_dgrad(qe_ctx *c, Plan &p, const LayerDev &L) {
+  if (L.desc.scaling != QE_SCALING_CURRENT) p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
 }
 
 void append_wgrad(Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, float *mg, int64_t offset, int64_t ld,
@@ -319,7 +355,8 @@ void *dev_alloc(qe_ctx *c, LayerDev &L, size_t bytes, bool *ok) {
 }
 
 bool meta_ok(const qe_fp8_meta *m) {
-  return m && m->amax_history && m->scale && m->scale_inv && m->history_len >= 1 &&
+  return m && m->amax_history && m->scale && m->scale_inv && uintptr_t(m->amax_accum) % 4 == 0 &&
+         m->history_len >= 1 &&
          m->history_len <= qe::kMaxHistory && valid_fmt(m->fmt);
 }
 
@@ -331,6 +368,7 @@ qe::MetaRef meta_ref(const qe_fp8_meta &m) {
   r.history_len = m.history_len;
   r.margin = m.margin;
   r.fmt = m.fmt;
+  r.accum = m.amax_accum;
   return r;
 }
 
@@ -388,6 +426,40 @@ qe_status qe_quantize_fp8(const void *in, qe_dtype in_dtype, int64_t rows, int64
   const qe::MetaRef m = meta_ref(*meta_host);
   const Call c = quant_call(in, in_dtype, rows, cols, m, q_row, ld_row, q_col, ld_col, scale_inv_snapshot);
   return qe::launch_quantize(c.q, static_cast<hipStream_t>(stream)) == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+qe_status qe_amax(const void *in, qe_dtype in_dtype, int64_t numel, const qe_fp8_meta *meta_host, qe_stream stream) {
+  if (!valid_dtype(in_dtype) || numel < 0 || !meta_ok(meta_host)) return QE_ERR_INVALID_ARG;
+  if (numel > 0 && in == nullptr) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(in) % (in_dtype == QE_BF16 ? 2 : 4) != 0) return QE_ERR_INVALID_ARG;
+  const qe::MetaRef m = meta_ref(*meta_host);
+  const qe::AmaxParams p = qe::amax_params(in, in_dtype == QE_BF16, numel, m.hist, m.accum);
+  return qe::launch_amax(p, static_cast<hipStream_t>(stream)) == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols,
+                                  const qe_fp8_meta *meta_host, uint8_t *q_row, int64_t ld_row, uint8_t *q_col,
+                                  int64_t ld_col, float *scale_inv_snapshot, int64_t *device_token,
+                                  qe_stream stream) {
+  if (!valid_dtype(in_dtype) || rows < 0 || cols < 0 || !meta_ok(meta_host) || meta_host->history_len != 1)
+    return QE_ERR_INVALID_ARG;
+  if (rows > 0 && cols > 0 && in == nullptr) return QE_ERR_INVALID_ARG;
+  if (q_row != nullptr && ld_row < cols) return QE_ERR_INVALID_ARG;
+  if (q_col != nullptr && ld_col < rows) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(in) % (in_dtype == QE_BF16 ? 2 : 4) != 0) return QE_ERR_INVALID_ARG;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const qe::MetaRef m = meta_ref(*meta_host);
+  const Call a = amax_call(in, in_dtype, rows * cols, m);
+  qe::UpdateParams u;
+  memset(&u, 0, sizeof(u));
+  u.m[0] = m;
+  u.n = 1;
+  u.token = reinterpret_cast<long long *>(device_token);
+  const Call q = quant_call(in, in_dtype, rows, cols, m, q_row, ld_row, q_col, ld_col, scale_inv_snapshot, false);
+  if (qe::launch_amax(a.a, s) != hipSuccess || qe::launch_scale_update(u, s) != hipSuccess ||
+      qe::launch_quantize(q.q, s) != hipSuccess)
+    return QE_ERR_HIP;
+  return QE_OK;
 }
 
 qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const uint8_t *b, qe_fp8_fmt fmt_b,
@@ -466,7 +538,10 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
       d->margin < -126 || d->margin > 252 || !valid_dtype(d->w_dtype) || !valid_fmt(d->fmt_x) ||
       !valid_fmt(d->fmt_w) || !valid_fmt(d->fmt_dy))
     return QE_ERR_INVALID_ARG;
+  if (d->scaling != QE_SCALING_DELAYED && d->scaling != QE_SCALING_CURRENT) return QE_ERR_INVALID_ARG;
+  if (d->scaling == QE_SCALING_CURRENT && d->history_len != 1) return QE_ERR_INVALID_ARG;
   if (!c->cfg.null_executor && d->w == nullptr) return QE_ERR_INVALID_ARG;
+  if (!elem_aligned(d->w, d->w_dtype)) return QE_ERR_INVALID_ARG;
   if (c->contract.has_layer(d->stage, d->unit)) return QE_ERR_INVALID_ARG;
   LayerDev L;
   L.desc = *d;
@@ -481,6 +556,7 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
     bool ok = true;
     const int H = d->history_len;
     L.meta = static_cast<float *>(dev_alloc(c, L, sizeof(float) * (3 * size_t(H) + 6), &ok));
+    L.accum = static_cast<float *>(dev_alloc(c, L, sizeof(float) * 3 * qe::kAmaxLines * qe::kAmaxStride, &ok));
     L.w_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->n_out) * L.ld_wq, &ok));
     L.w_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->k_in) * L.ld_wqt, &ok));
     L.w_sinv = static_cast<float *>(dev_alloc(c, L, sizeof(float), &ok));
@@ -522,6 +598,7 @@ qe_status qe_layer_meta(const qe_ctx *c, int32_t layer, qe_role role, qe_fp8_met
     out->amax_history = m.hist;
     out->scale = m.scale;
     out->scale_inv = m.scale_inv;
+    out->amax_accum = m.accum;
   }
   return QE_OK;
 }
@@ -560,6 +637,7 @@ qe_status qe_fp8_linear_fwd(qe_ctx *c, int32_t layer, qe_tape_key key, const voi
   if (c == nullptr || ref_out_host == nullptr || !valid_dtype(x_dtype) || !valid_dtype(y_dtype))
     return QE_ERR_INVALID_ARG;
   if (!c->cfg.null_executor && tokens > 0 && (x == nullptr || y == nullptr)) return QE_ERR_INVALID_ARG;
+  if (!elem_aligned(x, x_dtype) || !elem_aligned(y, y_dtype)) return QE_ERR_INVALID_ARG;
   bool refresh = false;
   const qe_status st = c->contract.check_fwd(layer, key, tokens, &refresh);
   if (st != QE_OK) return st;
@@ -582,12 +660,13 @@ qe_status qe_fp8_linear_dgrad(qe_ctx *c, int32_t layer, qe_tape_key key, qe_tape
   if (st != QE_OK) return st;
   const int64_t tokens = c->contract.layer(layer).slots[ref.slot].tokens;
   if (!c->cfg.null_executor && tokens > 0 && (dy == nullptr || dx == nullptr)) return QE_ERR_INVALID_ARG;
+  if (!elem_aligned(dy, dy_dtype) || !elem_aligned(dx, dx_dtype)) return QE_ERR_INVALID_ARG;
   if (c->contract.physical_fails()) return fail_physical(c);
   if (!c->cfg.null_executor) {
     const LayerDev &L = c->layers[size_t(layer)];
     Plan p;
     append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
-    p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+    finish_dgrad(c, p, L);
     if (run_plan(c, p, graph_key(layer, ACT_DGRAD, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
       return fail_physical(c);
   }
@@ -623,13 +702,14 @@ qe_status qe_fp8_linear_bwd_full(qe_ctx *c, int32_t layer, qe_tape_key key, qe_t
   if (st != QE_OK) return st;
   const int64_t tokens = c->contract.layer(layer).slots[ref.slot].tokens;
   if (!c->cfg.null_executor && tokens > 0 && (dy == nullptr || dx == nullptr)) return QE_ERR_INVALID_ARG;
+  if (!elem_aligned(dy, dy_dtype) || !elem_aligned(dx, dx_dtype)) return QE_ERR_INVALID_ARG;
   if (c->contract.physical_fails()) return fail_physical(c);
   if (!c->cfg.null_executor) {
     const LayerDev &L = c->layers[size_t(layer)];
     Plan p;
     append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
     append_wgrad(p, L, ref.slot, tokens, main_grad, offset, ld, mode);
-    p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+    finish_dgrad(c, p, L);
     if (run_plan(c, p, graph_key(layer, ACT_FULL, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
       return fail_physical(c);
   }

@@ -8,6 +8,8 @@ namespace qe {
 
 constexpr int kMaxMetas = 8;
 constexpr int kMaxHistory = 8192;
+constexpr int kAmaxLines = 64;   // amax accumulator: lines per role
+constexpr int kAmaxStride = 64;  // floats between lines (256 bytes)
 
 struct MetaRef {
   float *hist;
@@ -17,7 +19,19 @@ struct MetaRef {
   int32_t margin;
   int32_t fmt;
   int32_t pad;
+  float *accum;  // amax accumulator or null
 };
+
+// Fold a workgroup's max |x| (a float32 bit pattern, NaN above inf) into the
+// role's amax slot: line (workgroup % kAmaxLines) of the accumulator when
+// there is one, else the single float.  Called by one lane.
+__device__ __forceinline__ void fold_amax(float *accum, float *slot, uint32_t a) {
+  if (a == 0u) return;
+  if (accum != nullptr)
+    atomicMax(reinterpret_cast<unsigned int *>(accum + (blockIdx.x % kAmaxLines) * kAmaxStride), a);
+  else if (slot != nullptr)
+    atomicMax(reinterpret_cast<unsigned int *>(slot), a);
+}
 
 // Delayed scale update of n roles in one launch (one workgroup per role).
 struct UpdateParams {
@@ -35,7 +49,8 @@ struct QuantParams {
   int64_t rows, cols;
   const float *scale;
   const float *scale_inv;
-  float *amax_slot;  // history[0] of the role
+  float *amax_slot;   // history[0] of the role; null (with amax_accum null): nothing recorded
+  float *amax_accum;  // the role's amax accumulator, used instead of amax_slot when set
   uint8_t *q_row;
   int64_t ld_row;
   uint8_t *q_col;
@@ -67,11 +82,27 @@ struct GradCopyParams {
   int32_t pad;
 };
 
-enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COPY = 3, KC_COUNT = 4 };
+// *amax = max(*amax, max |in|) over numel contiguous elements (current scaling).
+// The tensor is split into `head` single elements before the first 16-byte
+// boundary, nvec 16-byte vectors from in + body_offset bytes, and `tail`
+// single elements from element tail_start (built by amax_params).
+struct AmaxParams {
+  const void *in;
+  float *amax;   // single float slot (used when accum is null)
+  float *accum;  // amax accumulator
+  int64_t body_offset, nvec, tail_start;
+  int32_t head, tail;
+  int32_t in_bf16;
+  int32_t pad;
+};
+
+enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COPY = 3, KC_AMAX = 4, KC_COUNT = 5 };
 
 hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s);
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
 hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s);
+hipError_t launch_amax(const AmaxParams &p, hipStream_t s);
+AmaxParams amax_params(const void *in, bool bf16, int64_t numel, float *amax, float *accum);
 
 }  // namespace qe

@@ -18,7 +18,8 @@
 // writes four 16-byte column segments; eight consecutive lanes complete one
 // 128-byte run of a transposed row.  amax: a max over the |x| bit patterns
 // (which order like the values, NaN above inf) per lane, a wave shuffle
-// reduction, then one atomicMax per workgroup.  HBM-bound: per element it
+// reduction, then one atomicMax per workgroup into one of the 64 lines of the
+// role's amax accumulator (same-line atomics serialise).  HBM-bound: per element it
 // moves 2 or 4 bytes in and 2 bytes out.
 #include "kernels.h"
 
@@ -199,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64
   if (tid == 0) {
     uint32_t a = red[0];
     for (int w = 1; w < kThreads / 64; ++w) a = red[w] > a ? red[w] : a;
-    if (a != 0u) atomicMax(reinterpret_cast<unsigned int *>(p.amax_slot), a);
+    fold_amax(p.amax_accum, p.amax_slot, a);
   }
 
   if (p.q_col == nullptr) return;

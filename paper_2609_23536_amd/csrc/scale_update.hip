@@ -37,9 +37,18 @@ __global__ __launch_bounds__(kThreads) void scale_update_kernel(UpdateParams p) 
 
   // amax values are >= +0 or a positive-signed NaN, so their bit patterns order
   // like the values, and every NaN pattern sorts above +inf.
+  // The role's amax accumulator (if any) is folded into history[0] and cleared.
+  uint32_t acc = 0;
+  if (m.accum != nullptr && tid < kAmaxLines) {
+    acc = __float_as_uint(m.accum[tid * kAmaxStride]) & 0x7fffffffu;
+    m.accum[tid * kAmaxStride] = 0.0f;
+  }
+  acc = wave_max_u32(acc);  // wave 0 holds the accumulator's value, the other waves 0
+
   uint32_t mx = 0;
   for (int i = tid; i < H; i += kThreads) {
     uint32_t b = __float_as_uint(m.hist[i]) & 0x7fffffffu;
+    if (i == 0) b = b > acc ? b : acc;  // i == 0 only on lane 0 of wave 0
     hist_sh[i] = b;
     mx = b > mx ? b : mx;
   }

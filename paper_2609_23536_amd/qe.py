@@ -19,7 +19,9 @@ E4M3, E5M2 = 0, 1
 F32, BF16 = 0, 1
 INIT, ACCUM = 0, 1
 ROLE_X, ROLE_W, ROLE_DY = 0, 1, 2
-KC_QUANT, KC_UPDATE, KC_GEMM, KC_COPY = 0, 1, 2, 3
+SCALING_DELAYED, SCALING_CURRENT = 0, 1
+AMAX_LINES, AMAX_STRIDE = 64, 64   # amax accumulator: lines x floats between lines
+KC_QUANT, KC_UPDATE, KC_GEMM, KC_COPY, KC_AMAX = 0, 1, 2, 3, 4
 
 STATUS = ["OK", "INVALID_ARG", "STALE_REF", "KEY_MISMATCH", "KEY_LIVE", "POOL_FULL", "DUPLICATE_CONSUMER", "ORDER",
           "EPOCH", "STALE_CACHE", "DEST_MISMATCH", "DEST_ALIAS", "DUP_WRITE", "ARENA_INVALID", "INCOMPLETE",
@@ -43,7 +45,8 @@ class TapeRef(C.Structure):
 
 class FP8Meta(C.Structure):
     _fields_ = [("amax_history", C.c_void_p), ("scale", C.c_void_p), ("scale_inv", C.c_void_p),
-                ("history_len", C.c_int32), ("margin", C.c_int32), ("fmt", C.c_int32), ("reserved", C.c_int32)]
+                ("history_len", C.c_int32), ("margin", C.c_int32), ("fmt", C.c_int32), ("reserved", C.c_int32),
+                ("amax_accum", C.c_void_p)]
 
 
 class Config(C.Structure):
@@ -56,7 +59,7 @@ class LayerDesc(C.Structure):
     _fields_ = [("stage", C.c_uint32), ("unit", C.c_uint32), ("n_out", C.c_int64), ("k_in", C.c_int64),
                 ("max_tokens", C.c_int64), ("w", C.c_void_p), ("w_dtype", C.c_int32), ("history_len", C.c_int32),
                 ("margin", C.c_int32), ("fmt_x", C.c_int32), ("fmt_w", C.c_int32), ("fmt_dy", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("scaling", C.c_int32)]
 
 
 class CtxState(C.Structure):
@@ -80,6 +83,8 @@ _P, _I32, _U32, _I64 = C.c_void_p, C.c_int32, C.c_uint32, C.c_int64
 _SIGS = {
     "qe_amax_scale_update": [C.POINTER(FP8Meta), _I32, _P, _P],
     "qe_quantize_fp8": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P],
+    "qe_amax": [_P, _I32, _I64, C.POINTER(FP8Meta), _P],
+    "qe_quantize_fp8_current": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P, _P],
     "qe_fp8_gemm_tn": [_P, _I32, _I64, _P, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _I32, _I64, _I32, _P],
     "qe_ctx_create": [C.POINTER(Config), C.POINTER(_P)],
     "qe_layer_register": [_P, C.POINTER(LayerDesc), C.POINTER(_I32)],
@@ -171,14 +176,26 @@ def qe_quantize_fp8(inp, in_dtype: int, rows: int, cols: int, meta: FP8Meta, q_r
                                      ld_col, ptr(scale_inv_snapshot), stream_handle(stream)))
 
 
+def qe_amax(inp, in_dtype: int, numel: int, meta: FP8Meta, stream=None) -> str:
+    return _st(lib().qe_amax(ptr(inp), in_dtype, numel, C.byref(meta), stream_handle(stream)))
+
+
+def qe_quantize_fp8_current(inp, in_dtype: int, rows: int, cols: int, meta: FP8Meta, q_row=None, ld_row: int = 0,
+                            q_col=None, ld_col: int = 0, scale_inv_snapshot=None, device_token=None,
+                            stream=None) -> str:
+    return _st(lib().qe_quantize_fp8_current(ptr(inp), in_dtype, rows, cols, C.byref(meta), ptr(q_row), ld_row,
+                                             ptr(q_col), ld_col, ptr(scale_inv_snapshot), ptr(device_token),
+                                             stream_handle(stream)))
+
+
 def qe_fp8_gemm_tn(a, fmt_a: int, lda: int, b, fmt_b: int, ldb: int, m: int, n: int, k: int, a_scale_inv,
                    b_scale_inv, c, c_dtype: int, ldc: int, mode: int = INIT, stream=None) -> str:
     return _st(lib().qe_fp8_gemm_tn(ptr(a), fmt_a, lda, ptr(b), fmt_b, ldb, m, n, k, ptr(a_scale_inv),
                                     ptr(b_scale_inv), ptr(c), c_dtype, ldc, mode, stream_handle(stream)))
 
 
-def make_meta(hist, scale, scale_inv, fmt: int, margin: int = 0) -> FP8Meta:
-    return FP8Meta(ptr(hist), ptr(scale), ptr(scale_inv), int(hist.numel()), margin, fmt, 0)
+def make_meta(hist, scale, scale_inv, fmt: int, margin: int = 0, amax_accum=None) -> FP8Meta:
+    return FP8Meta(ptr(hist), ptr(scale), ptr(scale_inv), int(hist.numel()), margin, fmt, 0, ptr(amax_accum))
 
 
 # --------------------------------------------------------------------------- context
@@ -209,9 +226,9 @@ class Context:
 
     def qe_layer_register(self, stage: int, unit: int, n_out: int, k_in: int, max_tokens: int, w, w_dtype: int,
                           history_len: int, margin: int, fmt_x: int = E4M3, fmt_w: int = E4M3,
-                          fmt_dy: int = E5M2):
+                          fmt_dy: int = E5M2, scaling: int = SCALING_DELAYED):
         d = LayerDesc(stage, unit, n_out, k_in, max_tokens, ptr(w), w_dtype, history_len, margin, fmt_x, fmt_w,
-                      fmt_dy, 0)
+                      fmt_dy, scaling)
         out = C.c_int32()
         return _st(lib().qe_layer_register(self.h, C.byref(d), C.byref(out))), out.value
 

@@ -30,9 +30,21 @@ def meta_buffer(H, device, scale=1.0):
     return b
 
 
-def meta_of(qe, buf, fmt, margin=0):
+def meta_of(qe, buf, fmt, margin=0, accum=None):
+    """FP8Meta over a meta_buffer; `accum` (64 x 64 float32, zeroed) adds an amax accumulator."""
     H = buf.numel() - 2
-    return qe.FP8Meta(buf.data_ptr(), buf.data_ptr() + 4 * H, buf.data_ptr() + 4 * (H + 1), H, margin, fmt, 0)
+    return qe.FP8Meta(buf.data_ptr(), buf.data_ptr() + 4 * H, buf.data_ptr() + 4 * (H + 1), H, margin, fmt, 0,
+                      0 if accum is None else accum.data_ptr())
+
+
+def accum_buffer(device):
+    return torch.zeros(64 * 64, dtype=torch.float32, device=device)
+
+
+def accum_value(accum):
+    """Value of an amax accumulator: max over its 64 lines (NaN if any line holds NaN)."""
+    lines = accum.cpu().numpy()[::64]
+    return float(np.nan) if np.isnan(lines).any() else float(lines.max())
 
 
 def rel_err(got, ref):

@@ -10,11 +10,11 @@ from tests.gpu_util import dev_bytes, dev_f32, torch, upload
 
 class Spec:
     def __init__(self, shapes, tokens, M, history, margin, in_dtype, shared_view, out_dtype="f32", seed=0,
-                 cfg=90, outliers=False):
+                 cfg=90, outliers=False, scaling="delayed"):
         self.shapes, self.tokens, self.M = shapes, tokens, M
         self.history, self.margin, self.in_dtype = history, margin, in_dtype
         self.shared_view, self.out_dtype, self.seed, self.cfg = shared_view, out_dtype, seed, cfg
-        self.outliers = outliers
+        self.outliers, self.scaling = outliers, scaling
 
     def total(self):
         return sum(n * k for n, k in self.shapes)
@@ -51,7 +51,9 @@ class GpuStage:
         dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
         self.w = [upload(spec.weight(u), self.d) for u in range(len(spec.shapes))]
         for u, (n, k) in enumerate(spec.shapes):
-            st, idx = self.ctx.qe_layer_register(0, u, n, k, spec.tokens, self.w[u], dt, spec.history, spec.margin)
+            rec = qe.SCALING_CURRENT if spec.scaling == "current" else qe.SCALING_DELAYED
+            st, idx = self.ctx.qe_layer_register(0, u, n, k, spec.tokens, self.w[u], dt, spec.history, spec.margin,
+                                                 scaling=rec)
             assert st == "OK" and idx == u
         self.grad = torch.zeros(spec.grad_elems(), dtype=torch.float32, device=self.d)
         for u, (n, k) in enumerate(spec.shapes):
@@ -142,7 +144,8 @@ class OracleStage:
         self.spec = spec
         self.st = Stage(spec.M)
         for u, (n, k) in enumerate(spec.shapes):
-            self.st.add_layer(0, u, spec.weight(u).as_f32(), spec.tokens, spec.history, spec.margin)
+            self.st.add_layer(0, u, spec.weight(u).as_f32(), spec.tokens, spec.history, spec.margin,
+                              scaling=spec.scaling)
         self.buf = 1 << 12
         self.st.add_buffer(self.buf, spec.grad_elems())
         for u, (n, k) in enumerate(spec.shapes):

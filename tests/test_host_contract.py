@@ -231,3 +231,14 @@ def test_random_schedules_match_oracle(seed):
         elif what == "rebuild":
             p.rebuild()
         p.check()
+
+
+def test_register_scaling_recipe_validation():
+    """Current scaling keeps no history: it needs history_len == 1; unknown recipes are rejected."""
+    qe = need_lib()
+    c = qe.Context(1, null_executor=True)
+    assert c.qe_layer_register(0, 0, 8, 8, 8, 0, qe.F32, 4, 0, scaling=qe.SCALING_CURRENT)[0] == "INVALID_ARG"
+    assert c.qe_layer_register(0, 0, 8, 8, 8, 0, qe.F32, 1, 0, scaling=2)[0] == "INVALID_ARG"
+    assert c.qe_layer_register(0, 0, 8, 8, 8, 0, qe.F32, 1, 0, scaling=qe.SCALING_CURRENT) == ("OK", 0)
+    assert c.qe_layer_register(0, 1, 8, 8, 8, 0, qe.F32, 4, 0, scaling=qe.SCALING_DELAYED) == ("OK", 1)
+    c.close()

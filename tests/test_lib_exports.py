@@ -1,6 +1,8 @@
 """The C ABI library loads without a GPU and exports every declared entry point."""
 import ctypes
 
+import pytest
+
 from tests.libqe import header_symbols, need_lib
 
 
@@ -22,11 +24,28 @@ def test_status_strings_match_binding():
 
 
 def test_struct_sizes():
+    """The binding's ctypes structs have the sizes the C compiler gives the header's structs."""
+    import os
+    import shutil
+    import subprocess
+    import tempfile
     qe = need_lib()
-    assert ctypes.sizeof(qe.TapeKey) == 20
-    assert ctypes.sizeof(qe.TapeRef) == 8
-    assert ctypes.sizeof(qe.FP8Meta) == 40
-    assert ctypes.sizeof(qe.LayerDesc) == 72
+    pairs = {"qe_tape_key": qe.TapeKey, "qe_tape_ref": qe.TapeRef, "qe_fp8_meta": qe.FP8Meta,
+             "qe_config": qe.Config, "qe_layer_desc": qe.LayerDesc, "qe_ctx_state": qe.CtxState,
+             "qe_layer_state": qe.LayerState, "qe_slot_state": qe.SlotState}
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    src = '#include <stdio.h>\n#include "qe.h"\nint main(void) {\n' + "".join(
+        f'  printf("{n} %zu\\n", sizeof({n}));\n' for n in pairs) + "  return 0;\n}\n"
+    with tempfile.TemporaryDirectory() as td:
+        c, exe = os.path.join(td, "sizes.c"), os.path.join(td, "sizes")
+        open(c, "w").write(src)
+        subprocess.run(["gcc", "-std=c99", "-I", inc, c, "-o", exe], check=True)
+        out = subprocess.run([exe], check=True, capture_output=True, text=True).stdout
+    sizes = dict((n, int(v)) for n, v in (line.split() for line in out.splitlines()))
+    for n, cls in pairs.items():
+        assert ctypes.sizeof(cls) == sizes[n], (n, ctypes.sizeof(cls), sizes[n])
 
 
 def test_invalid_args_rejected_without_device():
