@@ -25,6 +25,12 @@ State:
   are initialised by their first write and accumulated by later ones;
   overlapping views of different layers, or different views, are aliases
   (§3.4, §4.3).  A valid flag, cleared by an abort until rebuilt (§4.5).
+* Checkpoints (§3.5, Invariant 4): taken only at a quiescent point (no live
+  tape, no arena write since the last commit, a valid arena; Table "faults":
+  a checkpoint with live work is withheld).  e_W is persistent; tapes, slot
+  generations, the effect token and cache contents are process-local, so a
+  restore keeps this process's token and generations and marks every weight
+  cache stale, which makes the first forward refresh it.
 """
 from __future__ import annotations
 
@@ -300,6 +306,25 @@ class Contract:
         for b in self.bindings.values():
             b.written = False
         self.finalized = False
+        return OK
+
+    # ---------------------------------------------------------------- checkpoint
+    def checkpoint_check(self) -> str:
+        if any(s.live for L in self.layers for s in L.slots):
+            return NOT_QUIESCENT
+        if self.finalized or any(b.written for b in self.bindings.values()):
+            return NOT_QUIESCENT
+        if not self.arena_valid:
+            return ARENA_INVALID
+        return OK
+
+    def restore(self, e_w: int) -> str:
+        st = self.checkpoint_check()
+        if st != OK:
+            return st
+        self.e_w = int(e_w)
+        for L in self.layers:
+            L.e_c = -1
         return OK
 
     # ---------------------------------------------------------------- snapshot

@@ -21,6 +21,13 @@ and refreshed only in the first forward after an optimizer step).
 A layer with current (dynamic) scaling runs the same actions, but each tensor
 is cast with a scale set from its own amax just before the cast (X in F, W on
 a cache refresh, dY in dI); there is no history and nothing is recorded.
+
+A checkpoint (§3.5) is the persistent part of the stage: e_W, each layer's
+static configuration and precision recipe, and the FP8 state of its three
+roles.  The weight cache, tapes and token are rebuilt by the process that
+restores it; the restore marks the caches stale so the first forward
+re-quantizes W with the restored W scale, exactly as the first forward after
+any optimizer commit does.
 """
 from __future__ import annotations
 
@@ -50,6 +57,7 @@ class OracleLayer:
         if scaling not in ("delayed", "current"):
             raise ValueError(scaling)
         self.current = scaling == "current"
+        self.scaling, self.history, self.margin = scaling, int(history), int(margin)
         if self.current:
             self.sx = CurrentScaler(fmt_x, margin)
             self.sw = CurrentScaler(fmt_w, margin)
@@ -202,6 +210,48 @@ class Stage:
 
     def rebuild(self) -> str:
         return self.contract.rebuild()
+
+    # ---------------------------------------------------------------- checkpoint
+    def checkpoint_export(self):
+        """(status, payload): the persistent state, only at a quiescent point."""
+        st = self.contract.checkpoint_check()
+        if st != C.OK:
+            return st, None
+        layers = []
+        for info, L in zip(self.contract.layers, self.layers):
+            roles = {}
+            for r, s in (("x", L.sx), ("w", L.sw), ("dy", L.sdy)):
+                hist = np.zeros(1) if L.current else s.hist.copy()
+                roles[r] = (hist, s.scale, s.scale_inv)
+            layers.append({"stage": info.stage, "unit": info.unit, "n": info.n, "k": info.k,
+                           "max_tokens": info.max_tokens, "history": L.history, "margin": L.margin,
+                           "fmts": (L.fmt_x, L.fmt_w, L.fmt_dy), "scaling": L.scaling, "roles": roles})
+        return C.OK, {"e_w": self.contract.e_w, "microbatches": self.contract.M, "layers": layers}
+
+    def checkpoint_import(self, payload) -> str:
+        """Restore a payload into this process's stage, whose layers were
+        registered with the same configuration; nothing changes on a mismatch
+        or when the stage is not quiescent."""
+        if payload["microbatches"] != self.contract.M or len(payload["layers"]) != len(self.layers):
+            return C.INVALID_ARG
+        for p, info, L in zip(payload["layers"], self.contract.layers, self.layers):
+            mine = (info.stage, info.unit, info.n, info.k, info.max_tokens, L.history, L.margin,
+                    (L.fmt_x, L.fmt_w, L.fmt_dy), L.scaling)
+            theirs = (p["stage"], p["unit"], p["n"], p["k"], p["max_tokens"], p["history"], p["margin"],
+                      tuple(p["fmts"]), p["scaling"])
+            if mine != theirs:
+                return C.INVALID_ARG
+        st = self.contract.checkpoint_check()
+        if st != C.OK:
+            return st
+        for p, L in zip(payload["layers"], self.layers):
+            for r, s in (("x", L.sx), ("w", L.sw), ("dy", L.sdy)):
+                hist, scale, scale_inv = p["roles"][r]
+                if not L.current:
+                    s.hist = np.array(hist, dtype=np.float64)
+                s.scale, s.scale_inv = float(scale), float(scale_inv)
+            L.wq = L.wq_t = None
+        return self.contract.restore(payload["e_w"])
 
     def fp8_state(self, layer: int) -> dict:
         L = self.layers[layer]

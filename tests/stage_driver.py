@@ -44,12 +44,13 @@ class Spec:
 
 
 class GpuStage:
-    def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False):
+    def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False, weights=None):
+        """`weights`: the current master weights (workloads.Tensor per layer), default the initial ones."""
         self.qe, self.spec = qe, spec
         self.d = device
         self.ctx = qe.Context(spec.M, use_graphs=use_graphs, copy_gradients=copy_gradients)
         dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
-        self.w = [upload(spec.weight(u), self.d) for u in range(len(spec.shapes))]
+        self.w = [upload(spec.weight(u) if weights is None else weights[u], self.d) for u in range(len(spec.shapes))]
         for u, (n, k) in enumerate(spec.shapes):
             rec = qe.SCALING_CURRENT if spec.scaling == "current" else qe.SCALING_DELAYED
             st, idx = self.ctx.qe_layer_register(0, u, n, k, spec.tokens, self.w[u], dt, spec.history, spec.margin,
@@ -140,12 +141,13 @@ class GpuStage:
 
 
 class OracleStage:
-    def __init__(self, spec):
+    def __init__(self, spec, weights=None):
+        """`weights`: the current master weights (workloads.Tensor per layer), default the initial ones."""
         self.spec = spec
         self.st = Stage(spec.M)
         for u, (n, k) in enumerate(spec.shapes):
-            self.st.add_layer(0, u, spec.weight(u).as_f32(), spec.tokens, spec.history, spec.margin,
-                              scaling=spec.scaling)
+            w = spec.weight(u) if weights is None else weights[u]
+            self.st.add_layer(0, u, w.as_f32(), spec.tokens, spec.history, spec.margin, scaling=spec.scaling)
         self.buf = 1 << 12
         self.st.add_buffer(self.buf, spec.grad_elems())
         for u, (n, k) in enumerate(spec.shapes):
