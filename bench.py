@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the copied-gradient passes (direct placement only)")
     ap.add_argument("--no-current", action="store_true", help="skip the current-scaling passes")
+    ap.add_argument("--no-checkpoint", action="store_true", help="skip the checkpoint / restart measurement")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
@@ -235,9 +236,39 @@ def main():
     ms = el / args.steps * 1e3
     value = flops / (el / args.steps) / 1e12
 
+    # quiescent checkpoint at this optimizer boundary, restart into a fresh context
+    ckpt = None
+    if not args.no_checkpoint:
+        t0 = time.perf_counter()
+        cst, payload = b.ctx.qe_checkpoint_export()
+        export_ms = (time.perf_counter() - t0) * 1e3
+        assert cst == "OK", cst
+        epoch = b.epoch
     b.ctx.close()
     del b
     torch.cuda.empty_cache()
+    if not args.no_checkpoint:
+        r = StageBench(qe, torch, wl, use_graphs, dev)
+        r.epoch = epoch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        assert r.ctx.qe_checkpoint_import(payload) == "OK"
+        import_ms = (time.perf_counter() - t0) * 1e3
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r.step()                                  # graphs captured again, caches refreshed
+        torch.cuda.synchronize()
+        first_ms = (time.perf_counter() - t0) * 1e3
+        after_ms = timed_ms(r, torch, 0, 3)
+        assert r.ctx.qe_sync() == "OK"
+        rst = r.ctx.qe_get_state()
+        assert rst["device_token"] == rst["token"] and rst["e_w"] == epoch + 4
+        ckpt = {"payload_bytes": len(payload), "export_ms": round(export_ms, 3), "import_ms": round(import_ms, 3),
+                "first_step_after_restart_ms": round(first_ms, 3), "steady_step_after_restart_ms": round(after_ms, 4),
+                "graph_captures_after_restart": rst["captures"]}
+        r.ctx.close()
+        del r
+        torch.cuda.empty_cache()
 
     # ablation: the copied-gradient path (dW to a private buffer, then a copy
     # into the view) against direct placement, same steps, same replay mode
@@ -322,6 +353,8 @@ def main():
             "copies_per_step_direct": 0, "copies_per_step_copied": c_n // args.steps,
             "copy_bytes_per_step": copy_bytes, "copy_avg_launch_us": round(c_ms / c_n * 1e3, 2),
             "copy_achieved_gbs": round(copy_gbs, 1), "copy_frac_hbm": round(copy_gbs / HBM_PEAK_GBS, 4)}
+    if ckpt is not None:
+        out["checkpoint"] = ckpt
     if current_ms is not None:
         out["current_scaling"] = {
             "ms_per_step": round(current_ms, 4), "value": round(flops / (current_ms * 1e-3) / 1e12, 2),

@@ -307,6 +307,44 @@ qe_status qe_optimizer_commit(qe_ctx *ctx);
 qe_status qe_abort_epoch(qe_ctx *ctx);
 qe_status qe_arena_rebuild(qe_ctx *ctx);
 
+/* Quiescent checkpoint (§3.5, Invariant 4).  A checkpoint holds the
+ * persistent part of the stage: the logical optimizer epoch e_W, every
+ * registered layer's static configuration and precision recipe, and the FP8
+ * state (amax history, scale, scale_inv) of its three roles.  Tapes, slot
+ * generations, the effect token, graphs, events, arena bindings and the
+ * weight caches are process-local and are not in it.
+ *
+ * Payload (host bytes, little-endian, version 1): a 32-byte header {char
+ * magic[8] = "QECKPT01"; uint32 version; uint32 n_layers; int32 microbatches;
+ * int32 reserved; int64 e_w}; per layer a 64-byte record {uint32 stage, unit;
+ * int64 n_out, k_in, max_tokens; int32 w_dtype, history_len, margin, fmt_x,
+ * fmt_w, fmt_dy, scaling, reserved} followed, for the roles X, W, dY in that
+ * order, by history_len history floats, the scale and the scale_inv; then an
+ * 8-byte FNV-1a hash of all preceding bytes.
+ *
+ * Export: allowed only at a quiescent point: no live tape, and no arena write
+ * or finalize since the last qe_optimizer_commit (else QE_ERR_NOT_QUIESCENT;
+ * Table "faults": a checkpoint with live work is withheld), and a valid arena
+ * (else QE_ERR_ARENA_INVALID); nothing changes when refused.  It waits for
+ * the graph stream, then writes the payload.  *size_out_host always receives
+ * the payload size; with buf_host == NULL only the size is returned;
+ * capacity < size is QE_ERR_INVALID_ARG.  With null_executor the FP8 state
+ * written is the initial one (history 0, scales 1). */
+qe_status qe_checkpoint_export(qe_ctx *ctx, void *buf_host, int64_t capacity, int64_t *size_out_host);
+
+/* Import (restart): into a context whose layers were registered in the same
+ * order with the same configuration (stage, unit, n_out, k_in, max_tokens,
+ * w_dtype, history_len, margin, formats, scaling) and the same microbatch
+ * count, at a quiescent point.  Loads the FP8 state (clearing the amax
+ * accumulators), sets e_W to the saved epoch and marks every weight cache
+ * stale, so the first forward of the epoch (microbatch 0) re-quantizes W with
+ * the restored W scale; the token and generations stay this process's.
+ * Errors, with nothing changed: QE_ERR_INVALID_ARG (bad size, magic, version,
+ * hash, or a configuration that differs), QE_ERR_NOT_QUIESCENT /
+ * QE_ERR_ARENA_INVALID as for export.  QE_ERR_HIP: the device copy failed and
+ * the FP8 state is undefined; discard the context. */
+qe_status qe_checkpoint_import(qe_ctx *ctx, const void *buf_host, int64_t size);
+
 /* Block until all device work of the context has finished. */
 qe_status qe_sync(qe_ctx *ctx);
 

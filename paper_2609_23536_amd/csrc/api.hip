@@ -360,6 +360,61 @@ bool meta_ok(const qe_fp8_meta *m) {
          m->history_len <= qe::kMaxHistory && valid_fmt(m->fmt);
 }
 
+// ------------------------------------------------------------------ checkpoint payload
+constexpr char kCkptMagic[8] = {'Q', 'E', 'C', 'K', 'P', 'T', '0', '1'};
+constexpr uint32_t kCkptVersion = 1;
+
+struct CkptHeader {
+  char magic[8];
+  uint32_t version;
+  uint32_t n_layers;
+  int32_t microbatches;
+  int32_t reserved;
+  int64_t e_w;
+};
+struct CkptLayer {
+  uint32_t stage, unit;
+  int64_t n_out, k_in, max_tokens;
+  int32_t w_dtype, history_len, margin, fmt_x, fmt_w, fmt_dy, scaling, reserved;
+};
+static_assert(sizeof(CkptHeader) == 32 && sizeof(CkptLayer) == 64, "checkpoint record sizes");
+
+uint64_t fnv1a(const uint8_t *p, size_t n) {
+  uint64_t h = 1469598103934665603ull;
+  for (size_t i = 0; i < n; ++i) {
+    h ^= p[i];
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+CkptLayer ckpt_layer_of(const qe_layer_desc &d) {
+  CkptLayer r;
+  memset(&r, 0, sizeof(r));
+  r.stage = d.stage;
+  r.unit = d.unit;
+  r.n_out = d.n_out;
+  r.k_in = d.k_in;
+  r.max_tokens = d.max_tokens;
+  r.w_dtype = d.w_dtype;
+  r.history_len = d.history_len;
+  r.margin = d.margin;
+  r.fmt_x = d.fmt_x;
+  r.fmt_w = d.fmt_w;
+  r.fmt_dy = d.fmt_dy;
+  r.scaling = d.scaling;
+  return r;
+}
+
+// Payload bytes of the FP8 state of one layer: 3 roles x (H + 2) floats.
+size_t ckpt_state_bytes(const qe_layer_desc &d) { return sizeof(float) * 3 * (size_t(d.history_len) + 2); }
+
+int64_t ckpt_size(const std::vector<LayerDev> &layers) {
+  size_t n = sizeof(CkptHeader) + sizeof(uint64_t);
+  for (const auto &L : layers) n += sizeof(CkptLayer) + ckpt_state_bytes(L.desc);
+  return int64_t(n);
+}
+
 qe::MetaRef meta_ref(const qe_fp8_meta &m) {
   qe::MetaRef r{};
   r.hist = m.amax_history;
@@ -727,6 +782,99 @@ qe_status qe_arena_bind(qe_ctx *c, int32_t layer, uint32_t microbatch, float *bu
 qe_status qe_arena_finalize(qe_ctx *c) { return c ? c->contract.finalize() : QE_ERR_INVALID_ARG; }
 qe_status qe_optimizer_commit(qe_ctx *c) { return c ? c->contract.optimizer_commit() : QE_ERR_INVALID_ARG; }
 qe_status qe_arena_rebuild(qe_ctx *c) { return c ? c->contract.rebuild() : QE_ERR_INVALID_ARG; }
+
+qe_status qe_checkpoint_export(qe_ctx *c, void *buf_host, int64_t capacity, int64_t *size_out_host) {
+  if (c == nullptr || size_out_host == nullptr) return QE_ERR_INVALID_ARG;
+  const qe_status q = c->contract.checkpoint_check();
+  if (q != QE_OK) return q;
+  const int64_t size = ckpt_size(c->layers);
+  *size_out_host = size;
+  if (buf_host == nullptr) return QE_OK;
+  if (capacity < size) return QE_ERR_INVALID_ARG;
+  if (!c->cfg.null_executor && hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+  std::vector<uint8_t> out(size_t(size), 0);
+  uint8_t *w = out.data();
+  CkptHeader h;
+  memset(&h, 0, sizeof(h));
+  memcpy(h.magic, kCkptMagic, sizeof(h.magic));
+  h.version = kCkptVersion;
+  h.n_layers = uint32_t(c->layers.size());
+  h.microbatches = c->cfg.microbatches;
+  h.e_w = c->contract.e_w();
+  memcpy(w, &h, sizeof(h));
+  w += sizeof(h);
+  std::vector<float> meta;
+  for (const auto &L : c->layers) {
+    const CkptLayer r = ckpt_layer_of(L.desc);
+    memcpy(w, &r, sizeof(r));
+    w += sizeof(r);
+    const size_t H = size_t(L.desc.history_len);
+    meta.assign(3 * H + 6, 0.0f);  // hist[3][H] | scale[3] | scale_inv[3]
+    if (L.meta != nullptr) {
+      if (hipMemcpy(meta.data(), L.meta, sizeof(float) * meta.size(), hipMemcpyDeviceToHost) != hipSuccess)
+        return QE_ERR_HIP;
+    } else {
+      for (int k = 0; k < 6; ++k) meta[3 * H + size_t(k)] = 1.0f;  // null executor: initial state
+    }
+    for (size_t role = 0; role < 3; ++role) {
+      memcpy(w, meta.data() + role * H, sizeof(float) * H);
+      w += sizeof(float) * H;
+      memcpy(w, meta.data() + 3 * H + role, sizeof(float));
+      w += sizeof(float);
+      memcpy(w, meta.data() + 3 * H + 3 + role, sizeof(float));
+      w += sizeof(float);
+    }
+  }
+  const uint64_t hash = fnv1a(out.data(), size_t(w - out.data()));
+  memcpy(w, &hash, sizeof(hash));
+  memcpy(buf_host, out.data(), out.size());
+  return QE_OK;
+}
+
+qe_status qe_checkpoint_import(qe_ctx *c, const void *buf_host, int64_t size) {
+  if (c == nullptr || buf_host == nullptr || size != ckpt_size(c->layers)) return QE_ERR_INVALID_ARG;
+  const uint8_t *b = static_cast<const uint8_t *>(buf_host);
+  uint64_t hash = 0;
+  memcpy(&hash, b + size - int64_t(sizeof(hash)), sizeof(hash));
+  if (hash != fnv1a(b, size_t(size) - sizeof(hash))) return QE_ERR_INVALID_ARG;
+  CkptHeader h;
+  memcpy(&h, b, sizeof(h));
+  if (memcmp(h.magic, kCkptMagic, sizeof(h.magic)) != 0 || h.version != kCkptVersion ||
+      h.n_layers != uint32_t(c->layers.size()) || h.microbatches != c->cfg.microbatches || h.e_w < 0)
+    return QE_ERR_INVALID_ARG;
+  const uint8_t *r = b + sizeof(h);
+  for (const auto &L : c->layers) {  // configuration check before any change
+    CkptLayer got;
+    memcpy(&got, r, sizeof(got));
+    const CkptLayer mine = ckpt_layer_of(L.desc);
+    if (memcmp(&got, &mine, sizeof(got)) != 0) return QE_ERR_INVALID_ARG;
+    r += sizeof(got) + ckpt_state_bytes(L.desc);
+  }
+  const qe_status q = c->contract.checkpoint_check();
+  if (q != QE_OK) return q;
+  if (!c->cfg.null_executor) {
+    if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    r = b + sizeof(h);
+    std::vector<float> meta;
+    for (const auto &L : c->layers) {
+      r += sizeof(CkptLayer);
+      const size_t H = size_t(L.desc.history_len);
+      meta.assign(3 * H + 6, 0.0f);
+      for (size_t role = 0; role < 3; ++role) {
+        memcpy(meta.data() + role * H, r, sizeof(float) * H);
+        r += sizeof(float) * H;
+        memcpy(meta.data() + 3 * H + role, r, sizeof(float));
+        r += sizeof(float);
+        memcpy(meta.data() + 3 * H + 3 + role, r, sizeof(float));
+        r += sizeof(float);
+      }
+      if (hipMemcpy(L.meta, meta.data(), sizeof(float) * meta.size(), hipMemcpyHostToDevice) != hipSuccess ||
+          hipMemset(L.accum, 0, sizeof(float) * 3 * qe::kAmaxLines * qe::kAmaxStride) != hipSuccess)
+        return QE_ERR_HIP;
+    }
+  }
+  return c->contract.restore(h.e_w);
+}
 
 qe_status qe_abort_epoch(qe_ctx *c) {
   if (c == nullptr) return QE_ERR_INVALID_ARG;

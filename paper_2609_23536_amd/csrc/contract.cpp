@@ -235,4 +235,24 @@ qe_status Contract::rebuild() {
   return QE_OK;
 }
 
+qe_status Contract::checkpoint_check() const {
+  for (const auto &L : layers_)
+    for (const auto &s : L.slots)
+      if (s.live) return QE_ERR_NOT_QUIESCENT;
+  if (finalized_) return QE_ERR_NOT_QUIESCENT;
+  for (const auto &L : layers_)
+    for (const auto &v : L.views)
+      if (v.written) return QE_ERR_NOT_QUIESCENT;
+  if (!arena_valid_) return QE_ERR_ARENA_INVALID;
+  return QE_OK;
+}
+
+qe_status Contract::restore(int64_t e_w) {
+  const qe_status st = checkpoint_check();
+  if (st != QE_OK) return st;
+  e_w_ = e_w;
+  for (auto &L : layers_) L.e_c = -1;
+  return QE_OK;
+}
+
 }  // namespace qe

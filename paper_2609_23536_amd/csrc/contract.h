@@ -88,6 +88,11 @@ class Contract {
   void abort_epoch();
   qe_status rebuild();
 
+  // checkpoint (§3.5, Invariant 4): quiescence check, and the restart rule
+  // (persistent e_W, caches stale; tapes, generations and token kept local)
+  qe_status checkpoint_check() const;
+  qe_status restore(int64_t e_w);
+
   // fault injection: the n-th next physical action fails
   void inject_fault(int32_t n) { fail_countdown_ = n; }
   bool physical_fails();

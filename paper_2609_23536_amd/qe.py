@@ -101,6 +101,8 @@ _SIGS = {
     "qe_optimizer_commit": [_P],
     "qe_abort_epoch": [_P],
     "qe_arena_rebuild": [_P],
+    "qe_checkpoint_export": [_P, _P, _I64, C.POINTER(_I64)],
+    "qe_checkpoint_import": [_P, _P, _I64],
     "qe_sync": [_P],
     "qe_get_state": [_P, C.POINTER(CtxState)],
     "qe_get_layer_state": [_P, _I32, C.POINTER(LayerState)],
@@ -289,6 +291,20 @@ class Context:
 
     def qe_arena_rebuild(self) -> str:
         return _st(lib().qe_arena_rebuild(self.h))
+
+    def qe_checkpoint_export(self):
+        """(status, payload bytes or None)."""
+        size = C.c_int64()
+        st = _st(lib().qe_checkpoint_export(self.h, None, 0, C.byref(size)))
+        if st != "OK":
+            return st, None
+        buf = C.create_string_buffer(size.value)
+        st = _st(lib().qe_checkpoint_export(self.h, buf, size.value, C.byref(size)))
+        return (st, buf.raw[: size.value]) if st == "OK" else (st, None)
+
+    def qe_checkpoint_import(self, payload: bytes) -> str:
+        buf = C.create_string_buffer(payload, len(payload))
+        return _st(lib().qe_checkpoint_import(self.h, buf, len(payload)))
 
     def qe_sync(self) -> str:
         return _st(lib().qe_sync(self.h))

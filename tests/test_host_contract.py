@@ -120,6 +120,17 @@ class Pair:
         self.o.inject_fault(n)
         assert self.c.qe_inject_fault(n) == "OK"
 
+    def checkpoint(self):
+        st = self.o.checkpoint_check()
+        st_c, payload = self.c.qe_checkpoint_export()
+        assert st_c == st, ("checkpoint", st_c, st)
+        return st, payload
+
+    def restore(self, payload, e_w):
+        st = self.o.restore(e_w)
+        assert self.c.qe_checkpoint_import(payload) == st, ("restore", st)
+        return st
+
 
 def K(e, m, u=0, inv=0):
     return (e, 0, m, u, inv)
@@ -205,7 +216,7 @@ def test_random_schedules_match_oracle(seed):
             else OC.INIT
         if rng.random() < 0.05:
             mode = 1 - mode
-        what = rng.choice(["f", "f", "di", "dw", "full", "fin", "commit", "abort", "rebuild"])
+        what = rng.choice(["f", "f", "di", "dw", "full", "fin", "commit", "abort", "rebuild", "ckpt", "restore"])
         if what == "f":
             st, r = p.fwd(u, k, tokens=rng.randint(0, 16))
             if st == OC.OK:
@@ -230,6 +241,13 @@ def test_random_schedules_match_oracle(seed):
             p.abort()
         elif what == "rebuild":
             p.rebuild()
+        elif what == "ckpt":
+            e_w = p.o.e_w
+            st, payload = p.checkpoint()
+            if st == OC.OK:
+                refs["ckpt"] = (payload, e_w)
+        elif what == "restore" and "ckpt" in refs:
+            p.restore(*refs["ckpt"])
         p.check()
 
 
@@ -242,3 +260,77 @@ def test_register_scaling_recipe_validation():
     assert c.qe_layer_register(0, 0, 8, 8, 8, 0, qe.F32, 1, 0, scaling=qe.SCALING_CURRENT) == ("OK", 0)
     assert c.qe_layer_register(0, 1, 8, 8, 8, 0, qe.F32, 4, 0, scaling=qe.SCALING_DELAYED) == ("OK", 1)
     c.close()
+
+
+def _payload_fields(b):
+    import struct
+    magic, version, n_layers, M, _, e_w = struct.unpack_from("<8sIIiiq", b, 0)
+    return magic, version, n_layers, M, e_w
+
+
+def test_checkpoint_payload_and_validation():
+    """Payload layout and size, withheld checkpoints, and every rejected import
+    (bad hash, truncation, magic, version, other configuration, busy stage)
+    leaving the state unchanged."""
+    import struct
+    qe = need_lib()
+    p = Pair(2, [(4, 8, 16), (3, 5, 16)])
+    p.bind(0, 0, 0, 8)
+    p.bind(0, 1, 64, 8)
+    p.bind(1, 0, 128, 5)
+    p.bind(1, 1, 192, 5)
+    assert p.checkpoint()[0] == OC.OK
+    _, r = p.fwd(0, K(0, 0))
+    assert p.checkpoint() == (OC.NOT_QUIESCENT, None)                     # live tape
+    p.full(0, K(0, 0), r, 0, 8, OC.INIT)
+    assert p.checkpoint()[0] == OC.NOT_QUIESCENT                          # arena write in flight
+    for u in range(2):
+        for m in range(2):
+            if (u, m) != (0, 0):
+                _, r = p.fwd(u, K(0, m, u))
+                p.full(u, K(0, m, u), r, [0, 64, 128, 192][2 * u + m], [8, 5][u], OC.INIT)
+    assert p.finalize() == OC.OK
+    assert p.checkpoint()[0] == OC.NOT_QUIESCENT                          # finalized, not committed
+    assert p.commit() == OC.OK
+    st, payload = p.checkpoint()
+    assert st == OC.OK
+    assert len(payload) == 32 + 2 * (64 + 3 * (4 + 2) * 4) + 8
+    assert _payload_fields(payload) == (b"QECKPT01", 1, 2, 2, 1)
+    rec = struct.unpack_from("<IIqqqiiiiiiii", payload, 32)
+    assert rec == (0, 0, 4, 8, 16, qe.F32, 4, 0, qe.E4M3, qe.E4M3, qe.E5M2, qe.SCALING_DELAYED, 0)
+
+    def fresh():
+        q = Pair(2, [(4, 8, 16), (3, 5, 16)])
+        return q
+
+    bad = []
+    flipped = bytearray(payload)
+    flipped[40] ^= 1
+    bad.append(bytes(flipped))                                            # hash mismatch
+    bad.append(payload[:-1])                                              # truncated
+    for off, fmt, val in ((0, "<8s", b"QECKPT02"), (8, "<I", 2), (16, "<i", 3), (40, "<q", 9), (76, "<i", 5)):
+        b = bytearray(payload[:-8])
+        struct.pack_into(fmt, b, off, val)
+        bad.append(bytes(b) + _fnv1a(bytes(b)).to_bytes(8, "little"))    # well-formed hash, wrong field
+    for b in bad:
+        q = fresh()
+        snap = q.c.qe_get_state()
+        assert q.c.qe_checkpoint_import(b) == "INVALID_ARG"
+        assert q.c.qe_get_state() == snap
+    # a busy stage refuses the import
+    q = fresh()
+    _, r = q.fwd(0, K(0, 0))
+    assert q.c.qe_checkpoint_import(payload) == "NOT_QUIESCENT"
+    # the good payload restores e_W and marks the caches stale; token stays local
+    q = fresh()
+    assert q.restore(payload, 1) == OC.OK
+    q.check()
+    assert q.c.qe_get_state()["e_w"] == 1 and q.c.qe_get_state()["token"] == 0
+    assert q.c.qe_get_layer_state(0)["e_c"] == -1
+
+
+def _fnv1a(b):
+    h = 1469598103934665603
+    for x in b:
+        h = ((h ^ x) * 1099511628211) % (1 << 64)
+    return h
