@@ -17,7 +17,10 @@
 //    fragments feeds 16 MFMAs while the other set is read from LDS, and every
 //    fragment read or LDS-bound load is issued right after an MFMA, in a fixed
 //    order (sched_barrier), so the MFMA pipe stays busy in the single wave.
-//    The stage barrier sits between the two half-steps.  The epilogue goes
+//    The K loop is rotated (second half-step of tile t, then first half-step
+//    of tile t+1) so that its back-edge sits at the stage barrier, where all
+//    LDS reads have completed; the compiler can then wait for fragment reads
+//    one by one instead of draining them at the loop head.  The epilogue goes
 //    through LDS so every store instruction writes whole 512-byte row runs.
 //    Larger wave tiles mean less LDS traffic per FLOP than eight waves.
 //  * gemm_tn_kernel, 256 x 128 x 128 tiles: eight waves (two per SIMD) on a
@@ -74,11 +77,16 @@ __device__ __forceinline__ uint4 mask_tail(uint4 v, int64_t valid) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+// Two floats to two bf16 (round to nearest even, NaN stays a quiet NaN with
+// its sign and top payload bits) with the gfx950 packed conversion; bit-equal
+// to the integer form (u + 0x7fff + ((u >> 16) & 1)) >> 16 on every input,
+// which was checked on MI355X over all exponents, boundaries, denormals and NaNs.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
+__device__ __forceinline__ uint16_t bf16_bits(float f) { return uint16_t(bf16x2_bits(f, 0.0f)); }
 
 __device__ __forceinline__ int pow2_exponent(const float *p) { return int((__float_as_uint(*p) >> 23) & 0xffu) - 127; }
 
@@ -247,8 +255,8 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
         if constexpr (OUT == 0) {
           *reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col) = make_float4(v[0], v[1], v[2], v[3]);
         } else if constexpr (OUT == 1) {
-          const uint32_t lo = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
-          const uint32_t hi = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+          const uint32_t lo = bf16x2_bits(v[0], v[1]);
+          const uint32_t hi = bf16x2_bits(v[2], v[3]);
           *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(g.c) + row * g.ldc + col) = make_uint2(lo, hi);
         } else {
           float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col);
@@ -262,7 +270,7 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
           if constexpr (OUT == 0) {
             static_cast<float *>(g.c)[row * g.ldc + col + t] = v[t];
           } else if constexpr (OUT == 1) {
-            static_cast<uint16_t *>(g.c)[row * g.ldc + col + t] = uint16_t(f32_to_bf16_bits(v[t]));
+            static_cast<uint16_t *>(g.c)[row * g.ldc + col + t] = bf16_bits(v[t]);
           } else {
             float *dst = static_cast<float *>(g.c) + row * g.ldc + col + t;
             *dst = *dst + v[t];
@@ -425,33 +433,50 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
     __syncthreads();
     load_frags(0, 0, a0, b0);
     if (T > 1) issue(1, 1);
+    // first half of tile 0: MFMAs on set 0, reads of set 1 (tile 0, second half)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_one(q, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (q < 8) read_one(0, 1, q, a1, b1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();                       // tile 1 published; tile 0 fully read
+    // The loop is rotated so that its back-edge sits at the barrier, where every
+    // LDS read has completed anyway: the fragment reads of set 0 and their uses
+    // in the next half-step stay inside one iteration, and the waits for them
+    // can be partial instead of the full wait a loop header would need.
     for (int t = 0; t < T; ++t) {
       const int buf = t & 1;
-      const bool dma = t + 2 < KT;   // full tiles go LDS-bound, interleaved below
-      // first half: MFMAs on set 0, reads of set 1 (second half of tile t)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_one(q, a0, b0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (q < 8) {
-          read_one(buf, 1, q, a1, b1);
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();                     // tile t+1 published; tile t fully read
+      const bool dma = t + 2 < KT;
       if (t + 2 < T && !dma) issue(t + 2, buf);
-      // second half: MFMAs on set 1, loads of tile t+2, reads of set 0 (tile t+1)
+      // second half of tile t: MFMAs on set 1, loads of tile t+2, reads of set 0 (tile t+1)
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         __builtin_amdgcn_sched_barrier(0);
         mfma_one(q, a1, b1);
         __builtin_amdgcn_sched_barrier(0);
         if (dma) dma_one(t + 2, buf, q);
-        if (q >= 8 && t + 1 < T) read_one(buf ^ 1, 0, q - 8, a0, b0);
+        // unconditional: in the last iteration this reads a stale stage that
+        // is never used (always in bounds), and keeps the loop branch-free here
+        if (q >= 8) read_one(buf ^ 1, 0, q - 8, a0, b0);
       }
       __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < T) {
+        // first half of tile t+1: MFMAs on set 0, reads of set 1 (tile t+1, second half)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_one(q, a0, b0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (q < 8) read_one(buf ^ 1, 1, q, a1, b1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();                   // tile t+2 published; tile t+1 fully read
+      }
     }
   }
 
@@ -467,6 +492,19 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   const bool nfull = n0 + BN <= N;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
+    // accumulate: read this block's destination first, so the loads are in
+    // flight during the LDS round trip instead of one dependent load per row
+    float4 pre[16];
+    if constexpr (OUT == 2) {
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int64_t row = m0 + wm * TM + i * 32 + 2 * it + (lane >> 5);
+        const int64_t col = n0 + wn * TN + (lane & 31) * 4;
+        pre[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < M && vec_ok && (nfull || col + 4 <= N))
+          pre[it] = *reinterpret_cast<const float4 *>(static_cast<const float *>(g.c) + row * g.ldc + col);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -478,7 +516,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       }
     // same wave writes then reads its own LDS rows: LDS operations of one wave
     // complete in order
-#pragma unroll 4
+#pragma unroll
     for (int it = 0; it < 16; ++it) {
       const int r = 2 * it + (lane >> 5);
       const int64_t row = m0 + wm * TM + i * 32 + r;
@@ -491,13 +529,13 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
         if constexpr (OUT == 0) {
           *reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col) = v4;
         } else if constexpr (OUT == 1) {
-          const uint32_t lo = f32_to_bf16_bits(v[0]) | (f32_to_bf16_bits(v[1]) << 16);
-          const uint32_t hi = f32_to_bf16_bits(v[2]) | (f32_to_bf16_bits(v[3]) << 16);
+          const uint32_t lo = bf16x2_bits(v[0], v[1]);
+          const uint32_t hi = bf16x2_bits(v[2], v[3]);
           *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(g.c) + row * g.ldc + col) = make_uint2(lo, hi);
         } else {
-          float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col);
-          const float4 o = *dst;
-          *dst = make_float4(o.x + v[0], o.y + v[1], o.z + v[2], o.w + v[3]);
+          const float4 o = pre[it];
+          *reinterpret_cast<float4 *>(static_cast<float *>(g.c) + row * g.ldc + col) =
+              make_float4(o.x + v[0], o.y + v[1], o.z + v[2], o.w + v[3]);
         }
       } else {
 #pragma unroll
@@ -506,7 +544,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
           if constexpr (OUT == 0) {
             static_cast<float *>(g.c)[row * g.ldc + col + t] = v[t];
           } else if constexpr (OUT == 1) {
-            static_cast<uint16_t *>(g.c)[row * g.ldc + col + t] = uint16_t(f32_to_bf16_bits(v[t]));
+            static_cast<uint16_t *>(g.c)[row * g.ldc + col + t] = bf16_bits(v[t]);
           } else {
             float *dst = static_cast<float *>(g.c) + row * g.ldc + col + t;
             *dst = *dst + v[t];
