@@ -1,0 +1,320 @@
+"""Full-size parity on the remaining workloads, at their real shapes, in graph
+replay:
+
+* the zero-bubble-style schedule on the 8B-shaped stage (8 microbatches of
+  2048 tokens, forwards ahead of dI, deferred dW reversed then interleaved,
+  amax history 16 so it rolls over mid-step, 2 optimizer steps with a weight
+  update and version bump in between; every microbatch's dW accumulates into
+  one shared view per linear);
+* the outlier stress 8192^3 (0.1% of the input channels x300, log-normal(2)
+  gradients, margin 1, 3 steps: the first casts saturate, the scales back off);
+* the 70B-shaped stage at 8192 tokens, replayed 100 times.
+
+The oracle follows the delayed-scaling state exactly (amax of every full
+tensor, in action order) and checks it bit for bit; FP8 codes bit for bit on
+sampled rows / columns; Y, dX and the placed dW within tolerance on sampled
+blocks, computed from the quantized sampled rows and columns alone.  Inputs
+are the seeded recipes of workloads.py; the weight update between optimizer
+steps is W <- bf16(0.75 W), computed on the host from the previous weights.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import gemm, scaling
+from tests import schedules as S
+from tests.gpu_util import dev, dev_bytes, rel_err, torch, upload
+from tests.libqe import need_lib
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2.0 ** -8 + 1e-3
+
+
+def f32_of(t, rows=None, cols=None):
+    """float32 values of a workloads.Tensor, optionally of a row / column subset only."""
+    d = t.data
+    if rows is not None:
+        d = d[rows]
+    if cols is not None:
+        d = d[:, cols]
+    return W.bf16_bits_to_f32(d) if t.dtype == "bf16" else np.asarray(d, dtype=np.float32)
+
+
+def amax_of(t):
+    return scaling.amax(f32_of(t))
+
+
+def out_f32(buf):
+    a = buf.cpu().numpy()
+    return (a.view(np.uint16).astype(np.uint32) << 16).view(np.float32) if a.dtype == np.int16 else a
+
+
+class Tracker:
+    """The delayed-scaling state of every (layer, role), driven in action order
+    from full-tensor amaxes; remembers the scales each cast used."""
+
+    def __init__(self, n_layers, history, margin):
+        self.s = [{r: scaling.DelayedScaler(f, history, margin) for r, f in
+                   (("x", "E4M3"), ("w", "E4M3"), ("dy", "E5M2"))} for _ in range(n_layers)]
+        self.w_scale = [None] * n_layers     # (scale, scale_inv) of the weight cache
+        self.fwd_used = {}                   # (u, m, step) -> (x scale, x scale_inv)
+        self.dgrad_used = {}                 # (u, m, step) -> (dy scale, dy scale_inv)
+
+    def fwd(self, u, m, step, a_x, a_w=None):
+        L = self.s[u]
+        if a_w is not None:                  # cache refresh
+            self.w_scale[u] = (L["w"].scale, L["w"].scale_inv)
+            L["w"].record(a_w)
+        self.fwd_used[(u, m, step)] = (L["x"].scale, L["x"].scale_inv)
+        L["x"].record(a_x)
+        L["x"].update()
+        L["w"].update()
+
+    def dgrad(self, u, m, step, a_dy):
+        L = self.s[u]
+        self.dgrad_used[(u, m, step)] = (L["dy"].scale, L["dy"].scale_inv)
+        L["dy"].record(a_dy)
+        L["dy"].update()
+
+    def check_state(self, qe, ctx, d, u):
+        for name, role in (("x", qe.ROLE_X), ("w", qe.ROLE_W), ("dy", qe.ROLE_DY)):
+            ref = self.s[u][name]
+            m = ctx.qe_layer_meta(u, role)
+            H = len(ref.hist)
+            got = dev_bytes(m.amax_history, 4 * H, d).view(np.float32)
+            np.testing.assert_array_equal(got, ref.hist.astype(np.float32), err_msg=f"layer {u} {name} history")
+            assert dev_bytes(m.scale, 4, d).view(np.float32)[0] == np.float32(ref.scale), (u, name)
+            assert dev_bytes(m.scale_inv, 4, d).view(np.float32)[0] == np.float32(ref.scale_inv), (u, name)
+
+
+def check_cache(ctx, d, u, w, w_scale, J, n, k):
+    c = ctx.qe_layer_cache(u)
+    wq = dev_bytes(c["w_q"], n * c["ld_w_q"], d).reshape(n, c["ld_w_q"])[:, :k]
+    np.testing.assert_array_equal(wq[J], gemm.quantize(f32_of(w, rows=J), w_scale, "E4M3"), err_msg=f"W cache {u}")
+
+
+def check_y_dx(y, dx, x, dy, w, xs, ws, dys, I, J, Kk, fmt_dy="E5M2"):
+    """Y[I, J] and dX[I, Kk] against the oracle on quantized sampled rows / columns."""
+    xq = gemm.quantize(f32_of(x, rows=I), xs[0], "E4M3")
+    wq = gemm.quantize(f32_of(w, rows=J), ws[0], "E4M3")
+    y_ref = gemm.gemm_tn(xq, "E4M3", wq, "E4M3", xs[1], ws[1])
+    assert rel_err(out_f32(y)[np.ix_(I, J)], y_ref) <= BF16_TOL if y.dtype == torch.int16 else \
+        rel_err(out_f32(y)[np.ix_(I, J)], y_ref) <= 1e-3
+    dyq = gemm.quantize(f32_of(dy, rows=I), dys[0], fmt_dy)
+    wq_cols = gemm.quantize(f32_of(w, cols=Kk).T, ws[0], "E4M3")
+    dx_ref = gemm.gemm_tn(dyq, fmt_dy, wq_cols, "E4M3", dys[1], ws[1])
+    tol = BF16_TOL if dx.dtype == torch.int16 else 1e-3
+    assert rel_err(out_f32(dx)[np.ix_(I, Kk)], dx_ref) <= tol
+
+
+def dw_block(x, dy, xs, dys, J, Kk):
+    """dYq^T[J] (Xq^T)[Kk]^T of one microbatch, float64."""
+    a = gemm.quantize(f32_of(dy, cols=J).T, dys[0], "E5M2")
+    b = gemm.quantize(f32_of(x, cols=Kk).T, xs[0], "E4M3")
+    return gemm.gemm_tn(a, "E5M2", b, "E4M3", dys[1], xs[1])
+
+
+# ---------------------------------------------------------------------------------------- ZB
+@pytest.mark.timeout(600)
+def test_zero_bubble_8x2048_fullsize():
+    qe = need_lib()
+    d = dev()
+    wl = W.WORKLOADS["llama3_8b_zb_8x2048"]
+    M, t = wl.microbatches, wl.tokens
+    print("zb: generating inputs", flush=True)
+    ws = [W.layer_weight(wl, u) for u in range(len(wl.linears))]
+    inp = {(u, m): W.layer_inputs(wl, u, mb=m) for u in range(len(wl.linears)) for m in range(M)}
+    amax_x = {k: amax_of(v["x"]) for k, v in inp.items()}
+    amax_dy = {k: amax_of(v["dy"]) for k, v in inp.items()}
+    ctx = qe.Context(M, use_graphs=True)
+    dw_dev = [upload(w, d) for w in ws]
+    offs = wl.grad_offsets()
+    grad = torch.zeros(wl.flat_grad_elems(), dtype=torch.float32, device=d)
+    for u, lin in enumerate(wl.linears):
+        assert ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, t, dw_dev[u], qe.BF16, wl.history, wl.margin)[0] == "OK"
+        for m in range(M):                 # one shared view per linear: microbatches accumulate
+            assert ctx.qe_arena_bind(u, m, grad, grad.numel(), offs[u], lin.k_in) == "OK"
+    x_dev = {k: upload(v["x"], d) for k, v in inp.items()}
+    dy_dev = {k: upload(v["dy"], d) for k, v in inp.items()}
+    outs = {(u, m): (torch.empty((t, lin.n_out), dtype=torch.int16, device=d),
+                     torch.empty((t, lin.k_in), dtype=torch.int16, device=d))
+            for u, lin in enumerate(wl.linears) for m in range(M)}
+    tr = Tracker(len(wl.linears), wl.history, wl.margin)
+    rng = np.random.default_rng(7)
+    for step, sched in enumerate([S.ZB_STEP0, S.ZB_STEP1]):
+        print(f"zb: step {step}", flush=True)
+        S.check_legal(sched, M)
+        refs, written, dw_order = {}, set(), {u: [] for u in range(len(wl.linears))}
+        for a, m in sched:
+            for u, lin in enumerate(wl.linears):
+                key = qe.key(step, 0, m, u)
+                if a == "F":
+                    st, refs[(u, m)] = ctx.qe_fp8_linear_fwd(u, key, x_dev[(u, m)], qe.BF16, t, outs[(u, m)][0],
+                                                             qe.BF16)
+                    tr.fwd(u, m, step, amax_x[(u, m)], amax_of(ws[u]) if m == 0 else None)
+                elif a == "dI":
+                    st = ctx.qe_fp8_linear_dgrad(u, key, refs[(u, m)], dy_dev[(u, m)], qe.BF16, outs[(u, m)][1],
+                                                 qe.BF16)
+                    tr.dgrad(u, m, step, amax_dy[(u, m)])
+                else:
+                    mode = qe.ACCUM if u in written else qe.INIT
+                    st = ctx.qe_fp8_linear_wgrad_place(u, key, refs[(u, m)], grad, offs[u], lin.k_in, mode)
+                    written.add(u)
+                    dw_order[u].append(m)
+                assert st == "OK", (a, m, u, st)
+        torch.cuda.synchronize()
+        for u, lin in enumerate(wl.linears):
+            n, k = lin.n_out, lin.k_in
+            tr.check_state(qe, ctx, d, u)
+            J = np.sort(rng.choice(n, 16, replace=False))
+            Kk = np.sort(rng.choice(k, 16, replace=False))
+            I = np.sort(rng.choice(t, 16, replace=False))
+            check_cache(ctx, d, u, ws[u], tr.w_scale[u][0], J, n, k)
+            for m in (0, 5, M - 1):
+                check_y_dx(outs[(u, m)][0], outs[(u, m)][1], inp[(u, m)]["x"], inp[(u, m)]["dy"], ws[u],
+                           tr.fwd_used[(u, m, step)], tr.w_scale[u], tr.dgrad_used[(u, m, step)], I, J, Kk)
+            # the shared view: the 8 microbatch products, added in the order dW ran
+            ref = np.zeros((len(J), len(Kk)), dtype=np.float32)
+            for m in dw_order[u]:
+                blk = dw_block(inp[(u, m)]["x"], inp[(u, m)]["dy"], tr.fwd_used[(u, m, step)],
+                               tr.dgrad_used[(u, m, step)], J, Kk)
+                ref = (ref + blk.astype(np.float32)).astype(np.float32)
+            g = grad.cpu().numpy()
+            assert rel_err(g[offs[u] + J[:, None] * k + Kk[None, :]], ref) <= 1e-3, (u, step)
+        assert ctx.qe_arena_finalize() == "OK"
+        if step == 0:                      # optimizer step: W <- bf16(0.75 W), in place
+            for u in range(len(wl.linears)):
+                ws[u] = W.Tensor(W.f32_to_bf16_bits(f32_of(ws[u]) * np.float32(0.75)), "bf16")
+                dw_dev[u].copy_(upload(ws[u], d))
+        assert ctx.qe_optimizer_commit() == "OK"
+    assert ctx.qe_sync() == "OK"
+    st = ctx.qe_get_state()
+    assert st["device_token"] == st["token"] == 2 * 2 * M * len(wl.linears)
+    ctx.close()
+
+
+# ---------------------------------------------------------------------------------------- outliers
+@pytest.mark.timeout(600)
+def test_outlier_8192cube_fullsize():
+    qe = need_lib()
+    d = dev()
+    wl = W.WORKLOADS["outlier_8192cube"]
+    lin = wl.linears[0]
+    n, k, t = lin.n_out, lin.k_in, wl.tokens
+    print("outliers: generating inputs", flush=True)
+    w = W.layer_weight(wl, 0)
+    io = W.layer_inputs(wl, 0)
+    x, dy = io["x"], io["dy"]
+    a_x, a_w, a_dy = amax_of(x), amax_of(w), amax_of(dy)
+    ctx = qe.Context(1, use_graphs=True)
+    w_dev, x_dev, dy_dev = upload(w, d), upload(x, d), upload(dy, d)
+    assert ctx.qe_layer_register(0, 0, n, k, t, w_dev, qe.F32, wl.history, wl.margin)[0] == "OK"
+    grad = torch.zeros(n * k, dtype=torch.float32, device=d)
+    assert ctx.qe_arena_bind(0, 0, grad, grad.numel(), 0, k) == "OK"
+    y = torch.empty((t, n), dtype=torch.float32, device=d)
+    dx = torch.empty((t, k), dtype=torch.float32, device=d)
+    tr = Tracker(1, wl.history, wl.margin)
+    rng = np.random.default_rng(3)
+    saturated = 0
+    for step in range(wl.steps):
+        print(f"outliers: step {step}", flush=True)
+        key = qe.key(step, 0, 0, 0)
+        st, ref = ctx.qe_fp8_linear_fwd(0, key, x_dev, qe.F32, t, y, qe.F32)
+        assert st == "OK"
+        tr.fwd(0, 0, step, a_x, a_w)
+        assert ctx.qe_fp8_linear_dgrad(0, key, ref, dy_dev, qe.F32, dx, qe.F32) == "OK"
+        tr.dgrad(0, 0, step, a_dy)
+        assert ctx.qe_fp8_linear_wgrad_place(0, key, ref, grad, 0, k, qe.INIT) == "OK"
+        torch.cuda.synchronize()
+        tr.check_state(qe, ctx, d, 0)
+        xs, dys = tr.fwd_used[(0, 0, step)], tr.dgrad_used[(0, 0, step)]
+        I = np.sort(rng.choice(t, 24, replace=False))
+        J = np.sort(rng.choice(n, 24, replace=False))
+        # sampled columns include outlier channels: the ones with the largest |x|
+        big = np.argsort(-np.abs(f32_of(x, rows=np.arange(0, t, 512))).max(0))[:8]
+        Kk = np.unique(np.concatenate([big, rng.choice(k, 16, replace=False)]))
+        check_cache(ctx, d, 0, w, tr.w_scale[0][0], J, n, k)
+        p = ctx.qe_layer_slot_payload(0, 0)
+        xt = dev_bytes(p["x_q_t"], k * p["ld_x_q_t"], d).reshape(k, p["ld_x_q_t"])[:, :t]
+        dyt = dev_bytes(p["dy_q_t"], n * p["ld_dy_q_t"], d).reshape(n, p["ld_dy_q_t"])[:, :t]
+        want_x = gemm.quantize(f32_of(x, cols=Kk).T, xs[0], "E4M3")
+        np.testing.assert_array_equal(xt[Kk], want_x)
+        np.testing.assert_array_equal(dyt[J], gemm.quantize(f32_of(dy, cols=J).T, dys[0], "E5M2"))
+        saturated += int(np.sum((want_x & 0x7F) == 0x7E))
+        check_y_dx(y, dx, x, dy, w, xs, tr.w_scale[0], dys, I, J, Kk)
+        g = grad.cpu().numpy()
+        assert rel_err(g[J[:, None] * k + Kk[None, :]], dw_block(x, dy, xs, dys, J, Kk)) <= 1e-3
+        assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+    assert saturated > 0                    # the first step's casts did saturate
+    assert tr.s[0]["x"].scale < 1.0         # and the X scale backed off
+    ctx.close()
+
+
+# ---------------------------------------------------------------------------------------- 70B x 100
+@pytest.mark.timeout(900)
+def test_llama3_70b_stage_100_replays():
+    qe = need_lib()
+    d = dev()
+    wl = W.WORKLOADS["llama3_70b_stage_8192tok"]
+    t = wl.tokens
+    print("70b: generating inputs", flush=True)
+    ctx = qe.Context(1, use_graphs=True)
+    offs = wl.grad_offsets()
+    grad = torch.zeros(wl.flat_grad_elems(), dtype=torch.float32, device=d)
+    host, devs, outs = [], [], []
+    for u, lin in enumerate(wl.linears):
+        w = W.layer_weight(wl, u)
+        io = W.layer_inputs(wl, u)
+        host.append((w, io["x"], io["dy"], amax_of(w), amax_of(io["x"]), amax_of(io["dy"])))
+        devs.append((upload(w, d), upload(io["x"], d), upload(io["dy"], d)))
+        assert ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, t, devs[u][0], qe.BF16, wl.history,
+                                     wl.margin)[0] == "OK"
+        assert ctx.qe_arena_bind(u, 0, grad, grad.numel(), offs[u], lin.k_in) == "OK"
+        outs.append((torch.empty((t, lin.n_out), dtype=torch.int16, device=d),
+                     torch.empty((t, lin.k_in), dtype=torch.int16, device=d)))
+    tr = Tracker(len(wl.linears), wl.history, wl.margin)
+    snap = None
+    steps = 100
+    for step in range(steps):
+        refs = []
+        for u in range(len(wl.linears)):
+            st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(step, 0, 0, u), devs[u][1], qe.BF16, t, outs[u][0], qe.BF16)
+            assert st == "OK"
+            tr.fwd(u, 0, step, host[u][4], host[u][3])
+            refs.append(ref)
+        for u in reversed(range(len(wl.linears))):
+            key = qe.key(step, 0, 0, u)
+            assert ctx.qe_fp8_linear_dgrad(u, key, refs[u], devs[u][2], qe.BF16, outs[u][1], qe.BF16) == "OK"
+            tr.dgrad(u, 0, step, host[u][5])
+            assert ctx.qe_fp8_linear_wgrad_place(u, key, refs[u], grad, offs[u], wl.linears[u].k_in,
+                                                 qe.INIT) == "OK"
+        assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+        if step == 1:                       # the steady state: keep full copies to compare step 99 with
+            torch.cuda.synchronize()
+            snap = ([(o[0].clone(), o[1].clone()) for o in outs], grad.clone())
+        if step % 25 == 0:
+            print(f"70b: step {step}", flush=True)
+    torch.cuda.synchronize()
+    assert ctx.qe_sync() == "OK"
+    st = ctx.qe_get_state()
+    assert st["device_token"] == st["token"] == 2 * steps * len(wl.linears)
+    assert st["replays"] == 3 * steps * len(wl.linears)
+    # every replay after the scales settled reproduces step 1 bit for bit
+    for (y1, dx1), (y, dx) in zip(snap[0], outs):
+        assert torch.equal(y1, y) and torch.equal(dx1, dx)
+    assert torch.equal(snap[1], grad)
+    rng = np.random.default_rng(4)
+    g = grad.cpu().numpy()
+    for u, lin in enumerate(wl.linears):
+        n, k = lin.n_out, lin.k_in
+        tr.check_state(qe, ctx, d, u)
+        w, x, dy = host[u][0], host[u][1], host[u][2]
+        xs, dys = tr.fwd_used[(u, 0, steps - 1)], tr.dgrad_used[(u, 0, steps - 1)]
+        I = np.sort(rng.choice(t, 16, replace=False))
+        J = np.sort(rng.choice(n, 16, replace=False))
+        Kk = np.sort(rng.choice(k, 16, replace=False))
+        check_cache(ctx, d, u, w, tr.w_scale[u][0], J, n, k)
+        check_y_dx(outs[u][0], outs[u][1], x, dy, w, xs, tr.w_scale[u], dys, I, J, Kk)
+        assert rel_err(g[offs[u] + J[:, None] * k + Kk[None, :]], dw_block(x, dy, xs, dys, J, Kk)) <= 1e-3
+    ctx.close()
