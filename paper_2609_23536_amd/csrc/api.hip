@@ -16,6 +16,7 @@
 
 #include <chrono>
 #include <map>
+#include <new>
 #include <vector>
 
 #include "../../include/qe.h"
@@ -25,6 +26,27 @@
 namespace {
 
 int64_t rup16(int64_t v) { return (v + 15) / 16 * 16; }
+
+// Makes the context's device current for the scope of one call and restores
+// the caller's device afterwards.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) {
+      prev = -1;
+      ok = false;
+      return;
+    }
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+  DeviceGuard(const DeviceGuard &) = delete;
+  DeviceGuard &operator=(const DeviceGuard &) = delete;
+};
 
 struct Call {
   int32_t kind;  // qe::KernelClass
@@ -155,6 +177,8 @@ hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed) {
 
 // Two-way handoff around one action (§2.3, §4.4).
 qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller) {
+  DeviceGuard dg(c->cfg.device);
+  if (!dg.ok) return QE_ERR_HIP;
   if (caller != c->gs) {
     if (hipEventRecord(c->ev_in, caller) != hipSuccess) return QE_ERR_HIP;
     if (hipStreamWaitEvent(c->gs, c->ev_in, 0) != hipSuccess) return QE_ERR_HIP;
@@ -539,12 +563,14 @@ qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
   if (cfg_host == nullptr || out_host == nullptr || cfg_host->microbatches < 1 || cfg_host->microbatches > 4096)
     return QE_ERR_INVALID_ARG;
   *out_host = nullptr;
-  qe_ctx *c = new qe_ctx(*cfg_host);
+  qe_ctx *c = new (std::nothrow) qe_ctx(*cfg_host);
+  if (c == nullptr) return QE_ERR_HIP;
   c->st.device_token = -1;
   c->st.arena_valid = 1;
   if (!c->cfg.null_executor) {
     hipDeviceProp_t prop;
-    if (hipSetDevice(c->cfg.device) != hipSuccess || hipGetDeviceProperties(&prop, c->cfg.device) != hipSuccess) {
+    DeviceGuard dg(c->cfg.device);
+    if (!dg.ok || hipGetDeviceProperties(&prop, c->cfg.device) != hipSuccess) {
       delete c;
       return QE_ERR_HIP;
     }
@@ -569,6 +595,7 @@ qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
 void qe_ctx_destroy(qe_ctx *c) {
   if (c == nullptr) return;
   if (!c->cfg.null_executor) {
+    DeviceGuard dg(c->cfg.device);
     if (c->gs) (void)hipStreamSynchronize(c->gs);
     for (auto &kv : c->graphs)
       if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
@@ -608,6 +635,9 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
   L.ld_dyq = rup16(d->n_out);
   L.ld_t = rup16(d->max_tokens);
   if (!c->cfg.null_executor) {
+    DeviceGuard dg(c->cfg.device);
+    if (!dg.ok) return QE_ERR_HIP;
+    const int64_t bytes_before = c->st.device_bytes;
     bool ok = true;
     const int H = d->history_len;
     L.meta = static_cast<float *>(dev_alloc(c, L, sizeof(float) * (3 * size_t(H) + 6), &ok));
@@ -632,6 +662,7 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
     }
     if (!ok) {
       for (void *p : L.allocs) (void)hipFree(p);
+      c->st.device_bytes = bytes_before;
       return QE_ERR_HIP;
     }
   }
@@ -791,7 +822,8 @@ qe_status qe_checkpoint_export(qe_ctx *c, void *buf_host, int64_t capacity, int6
   *size_out_host = size;
   if (buf_host == nullptr) return QE_OK;
   if (capacity < size) return QE_ERR_INVALID_ARG;
-  if (!c->cfg.null_executor && hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+  DeviceGuard dg(c->cfg.device);
+  if (!c->cfg.null_executor && (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess)) return QE_ERR_HIP;
   std::vector<uint8_t> out(size_t(size), 0);
   uint8_t *w = out.data();
   CkptHeader h;
@@ -853,7 +885,8 @@ qe_status qe_checkpoint_import(qe_ctx *c, const void *buf_host, int64_t size) {
   const qe_status q = c->contract.checkpoint_check();
   if (q != QE_OK) return q;
   if (!c->cfg.null_executor) {
-    if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    DeviceGuard dg(c->cfg.device);
+    if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
     r = b + sizeof(h);
     std::vector<float> meta;
     for (const auto &L : c->layers) {
@@ -885,7 +918,8 @@ qe_status qe_abort_epoch(qe_ctx *c) {
 qe_status qe_sync(qe_ctx *c) {
   if (c == nullptr) return QE_ERR_INVALID_ARG;
   if (c->cfg.null_executor) return QE_OK;
-  if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+  DeviceGuard dg(c->cfg.device);
+  if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
   long long tok = 0;
   if (hipMemcpy(&tok, c->d_token, sizeof(tok), hipMemcpyDeviceToHost) != hipSuccess) return QE_ERR_HIP;
   c->st.device_token = tok;
@@ -951,7 +985,8 @@ qe_status qe_get_kernel_timing(qe_ctx *c, int32_t kernel_class, double *total_ms
   if (c == nullptr || kernel_class < 0 || kernel_class >= qe::KC_COUNT || !total_ms_host || !launches_host)
     return QE_ERR_INVALID_ARG;
   if (!c->cfg.null_executor && !c->timed.empty()) {
-    if (hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    DeviceGuard dg(c->cfg.device);
+    if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
     for (auto &t : c->timed) {
       float ms = 0.f;
       if (hipEventElapsedTime(&ms, t.t0, t.t1) != hipSuccess) return QE_ERR_HIP;
