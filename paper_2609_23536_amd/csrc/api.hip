@@ -579,7 +579,11 @@ qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
       return QE_ERR_UNSUPPORTED;
     }
     bool ok = hipStreamCreateWithFlags(&c->gs, hipStreamNonBlocking) == hipSuccess;
-    ok = ok && hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming) == hipSuccess;
+    // The caller -> graph edge is only ever consumed by kernels on this device,
+    // so a device-scope release is enough there (saves ~2 us per action on
+    // MI355X).  The graph -> caller edge keeps the system-scope release: after
+    // it the caller may hand results to the host or to a copy engine.
+    ok = ok && hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming | hipEventDisableSystemFence) == hipSuccess;
     ok = ok && hipEventCreateWithFlags(&c->ev_tail, hipEventDisableTiming) == hipSuccess;
     ok = ok && hipMalloc(reinterpret_cast<void **>(&c->d_token), sizeof(long long)) == hipSuccess;
     ok = ok && hipMemset(c->d_token, 0, sizeof(long long)) == hipSuccess;
