@@ -45,6 +45,8 @@ def parse():
                     help="skip the copied-gradient passes (direct placement only)")
     ap.add_argument("--no-current", action="store_true", help="skip the current-scaling passes")
     ap.add_argument("--no-checkpoint", action="store_true", help="skip the checkpoint / restart measurement")
+    ap.add_argument("--no-latency", action="store_true",
+                    help="skip the per-action latency of the small single-linear schedule")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
@@ -133,6 +135,69 @@ class StageBench:
         assert ctx.qe_arena_finalize() == "OK"
         assert ctx.qe_optimizer_commit() == "OK"
         self.epoch += 1
+
+
+def per_action_latency(qe, torch, device, steps=200, warmup=10):
+    """Latency-bound case: one FP8 linear (K = N = 256), two microbatches of 128
+    tokens, fp32 inputs, history 4, schedule F0 F1 dI0 dI1 dW0 dW1 (both dW into
+    one shared view: INIT, then ACCUM), then finalize and commit.  Mean wall time
+    per action, graph replay behind the two-way handoff vs direct launches."""
+    import numpy as np
+    import workloads as W
+    wl = W.WORKLOADS["single_linear_128x256x256"]
+    lin = wl.linears[0]
+
+    def up(t):
+        return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
+
+    res = {}
+    for mode in ("graph", "eager"):
+        ctx = qe.Context(wl.microbatches, use_graphs=(mode == "graph"))
+        w = up(W.layer_weight(wl, 0))
+        st, idx = ctx.qe_layer_register(0, 0, lin.n_out, lin.k_in, wl.tokens, w, qe.F32, wl.history, wl.margin)
+        assert st == "OK" and idx == 0, st
+        grad = torch.zeros(lin.n_out * lin.k_in, dtype=torch.float32, device=device)
+        for m in range(wl.microbatches):
+            assert ctx.qe_arena_bind(0, m, grad, grad.numel(), 0, lin.k_in) == "OK"
+        xs = [up(W.layer_inputs(wl, 0, mb=m)["x"]) for m in range(wl.microbatches)]
+        dys = [up(W.layer_inputs(wl, 0, mb=m)["dy"]) for m in range(wl.microbatches)]
+        ys = [torch.empty((wl.tokens, lin.n_out), dtype=torch.float32, device=device) for _ in xs]
+        dxs = [torch.empty((wl.tokens, lin.k_in), dtype=torch.float32, device=device) for _ in xs]
+        epoch = [0]
+
+        def step():
+            refs = []
+            for m in range(wl.microbatches):
+                st, ref = ctx.qe_fp8_linear_fwd(0, qe.key(epoch[0], 0, m, 0), xs[m], qe.F32, wl.tokens, ys[m], qe.F32)
+                assert st == "OK", st
+                refs.append(ref)
+            for m in range(wl.microbatches):
+                st = ctx.qe_fp8_linear_dgrad(0, qe.key(epoch[0], 0, m, 0), refs[m], dys[m], qe.F32, dxs[m], qe.F32)
+                assert st == "OK", st
+            for m in range(wl.microbatches):
+                st = ctx.qe_fp8_linear_wgrad_place(0, qe.key(epoch[0], 0, m, 0), refs[m], grad, 0, lin.k_in,
+                                                   qe.INIT if m == 0 else qe.ACCUM)
+                assert st == "OK", st
+            assert ctx.qe_arena_finalize() == "OK"
+            assert ctx.qe_optimizer_commit() == "OK"
+            epoch[0] += 1
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        assert ctx.qe_sync() == "OK"
+        stt = ctx.qe_get_state()
+        assert stt["device_token"] == stt["token"]
+        res[mode] = el / (steps * 3 * wl.microbatches) * 1e6
+        ctx.close()
+    return {"workload": wl.key, "actions_per_step": 3 * wl.microbatches,
+            "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
+            "eager_over_graph": round(res["eager"] / res["graph"], 3)}
 
 
 def timed_ms(b, torch, warmup, steps):
@@ -292,6 +357,8 @@ def main():
         del c
         torch.cuda.empty_cache()
 
+    latency = None if args.no_latency else per_action_latency(qe, torch, dev)
+
     # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
     def instrumented(copy_gradients=False, current=False):
         e = StageBench(qe, torch, wl, False, dev, copy_gradients=copy_gradients, current=current)
@@ -364,6 +431,8 @@ def main():
                      "launches": a_n, "bytes_per_step": amax_bytes(wl)},
             "quantize": {"achieved": round(cq_gbs, 1), "unit": "GB/s", "frac": round(cq_gbs / HBM_PEAK_GBS, 4),
                          "avg_launch_us": round(cq_ms / cq_n * 1e3, 2), "launches": cq_n}}
+    if latency is not None:
+        out["per_action_latency"] = latency
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
     print(json.dumps(out), flush=True)
