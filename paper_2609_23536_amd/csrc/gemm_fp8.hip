@@ -54,6 +54,8 @@ namespace qe {
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 128;
@@ -490,32 +492,70 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   float *ep = reinterpret_cast<float *>(smem) + wave * 32 * EP;
   const int e = pow2_exponent(g.a_scale_inv) + pow2_exponent(g.b_scale_inv);
   const bool nfull = n0 + BN <= N;
+  // Full tile with a vector-aligned destination (the common case): no bounds
+  // checks, every store address is a uniform row base (scalar registers) plus
+  // one per-lane offset, and LDS addresses are one base plus immediates.  With
+  // one wave per SIMD the epilogue runs at instruction latency, so its
+  // instruction count is its time.  Other tiles take the checked path.
+  constexpr int ES = OUT == 1 ? 2 : 4;  // output element bytes
+  // (buffer instructions: the row offset is a scalar operand; every offset of
+  // the wave's 128 x 128 block stays below 2^31)
+  const bool fast = vec_ok && nfull && m0 + BM <= M && g.ldc * ES * (TM + 2) < (int64_t(1) << 31);
+  const int wu = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t voff = uint32_t((lane >> 5) * g.ldc + (lane & 31) * 4) * uint32_t(ES);
+  char *cbase = static_cast<char *>(g.c) + ((m0 + (wu >> 1) * TM) * g.ldc + n0 + (wu & 1) * TN) * ES;
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(cbase, short(0), 0x7fffffff, 0x00020000);
+  const int rstep = int(g.ldc) * ES;  // bytes per output row
+  float *ew = ep + (lane & 31) * EP + 4 * (lane >> 5);
+  const float *er = ep + (lane >> 5) * EP + (lane & 31) * 4;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     // accumulate: read this block's destination first, so the loads are in
     // flight during the LDS round trip instead of one dependent load per row
     float4 pre[16];
     if constexpr (OUT == 2) {
+      if (fast) {
 #pragma unroll
-      for (int it = 0; it < 16; ++it) {
-        const int64_t row = m0 + wm * TM + i * 32 + 2 * it + (lane >> 5);
-        const int64_t col = n0 + wn * TN + (lane & 31) * 4;
-        pre[it] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row < M && vec_ok && (nfull || col + 4 <= N))
-          pre[it] = *reinterpret_cast<const float4 *>(static_cast<const float *>(g.c) + row * g.ldc + col);
+        for (int it = 0; it < 16; ++it)
+          pre[it] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, (i * 32 + 2 * it) * rstep, 0));
+      } else {
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+          const int64_t row = m0 + wm * TM + i * 32 + 2 * it + (lane >> 5);
+          const int64_t col = n0 + wn * TN + (lane & 31) * 4;
+          pre[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (row < M && vec_ok && (nfull || col + 4 <= N))
+            pre[it] = *reinterpret_cast<const float4 *>(static_cast<const float *>(g.c) + row * g.ldc + col);
+        }
       }
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = j * 32 + 8 * q + 4 * (lane >> 5);
-        *reinterpret_cast<float4 *>(ep + (lane & 31) * EP + col) =
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4 *>(ew + j * 32 + 8 * q) =
             make_float4(__builtin_ldexpf(acc[i][j][4 * q], e), __builtin_ldexpf(acc[i][j][4 * q + 1], e),
                         __builtin_ldexpf(acc[i][j][4 * q + 2], e), __builtin_ldexpf(acc[i][j][4 * q + 3], e));
-      }
     // same wave writes then reads its own LDS rows: LDS operations of one wave
     // complete in order
+    if (fast) {
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const float4 v4 = *reinterpret_cast<const float4 *>(er + it * 2 * EP);
+        const int so = (i * 32 + 2 * it) * rstep;
+        if constexpr (OUT == 0) {
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v4), crs, voff, so, 0);
+        } else if constexpr (OUT == 1) {
+          const v2i w = {int(bf16x2_bits(v4.x, v4.y)), int(bf16x2_bits(v4.z, v4.w))};
+          __builtin_amdgcn_raw_buffer_store_b64(w, crs, voff, so, 0);
+        } else {
+          const float4 o = pre[it];
+          const float4 r = make_float4(o.x + v4.x, o.y + v4.y, o.z + v4.z, o.w + v4.w);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, r), crs, voff, so, 0);
+        }
+      }
+      continue;
+    }
 #pragma unroll
     for (int it = 0; it < 16; ++it) {
       const int r = 2 * it + (lane >> 5);
