@@ -243,6 +243,41 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   // epilogue: lane holds rows (lane & 15), columns 4*(lane >> 4) .. +3 of each 16x16 block
   const int e = pow2_exponent(g.a_scale_inv) + pow2_exponent(g.b_scale_inv);
   const bool mfull = m0 + BM <= M, nfull = n0 + BN <= N;
+  // Full tile, vector-aligned destination: buffer stores (and accumulate
+  // loads) at a scalar block offset plus one fixed per-lane offset, with no
+  // bounds checks; every offset stays below 2^31.  Edge tiles take the checked
+  // path below.
+  constexpr int ES = OUT == 1 ? 2 : 4;  // output element bytes
+  if (vec_ok && mfull && nfull && g.ldc * ES * (BM + 1) < (int64_t(1) << 31)) {
+    const int wu = __builtin_amdgcn_readfirstlane(wave);
+    const int wmu = wu / WN, wnu = wu % WN;
+    const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+        static_cast<char *>(g.c) + (m0 * g.ldc + n0) * ES, short(0), 0x7fffffff, 0x00020000);
+    const uint32_t voff = uint32_t((lane & 15) * g.ldc + 4 * (lane >> 4)) * uint32_t(ES);
+    const int rstep = int(g.ldc) * ES;
+#pragma unroll
+    for (int i = 0; i < FI; ++i)
+#pragma unroll
+      for (int j = 0; j < FJ; ++j) {
+        const int so = (wmu * TM + i * 16) * rstep + (wnu * TN + j * 16) * ES;
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = __builtin_ldexpf(acc[i][j][t], e);
+        if constexpr (OUT == 0) {
+          const v4i w = {__builtin_bit_cast(int, v[0]), __builtin_bit_cast(int, v[1]), __builtin_bit_cast(int, v[2]),
+                         __builtin_bit_cast(int, v[3])};
+          __builtin_amdgcn_raw_buffer_store_b128(w, crs, voff, so, 0);
+        } else if constexpr (OUT == 1) {
+          const v2i w = {int(bf16x2_bits(v[0], v[1])), int(bf16x2_bits(v[2], v[3]))};
+          __builtin_amdgcn_raw_buffer_store_b64(w, crs, voff, so, 0);
+        } else {
+          const float4 o = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, so, 0));
+          const float4 r = make_float4(o.x + v[0], o.y + v[1], o.z + v[2], o.w + v[3]);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, r), crs, voff, so, 0);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < FI; ++i) {
     const int64_t row = m0 + wm * TM + i * 16 + (lane & 15);
