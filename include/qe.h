@@ -182,6 +182,25 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
                          const float *b_scale_inv, void *c, qe_dtype c_dtype, int64_t ldc, qe_place_mode mode,
                          qe_stream stream);
 
+/* Macro-tile shape of every FP8 GEMM the library launches (qe_fp8_gemm_tn and
+ * the layer actions).  QE_TILE_AUTO picks, per call, the shape that needs the
+ * fewest rounds of workgroups over the 256 compute units, weighted by a
+ * measured per-round cost; the others force one shape (for tests and
+ * measurements).  Process-wide; it applies to launches enqueued afterwards
+ * (a graph captured earlier keeps the shapes it was captured with).  The
+ * three 4-wave shapes (256x256, 256x192, 192x256) give the same bits: the same
+ * 32x32x64 MFMA and the same order along K, no split reduction.  256x128 uses
+ * the 16x16x128 MFMA and may differ from them in the last bits.
+ * Errors: QE_ERR_INVALID_ARG for a value outside the enum. */
+typedef enum {
+  QE_TILE_AUTO = 0,
+  QE_TILE_256x256 = 1,
+  QE_TILE_256x192 = 2,
+  QE_TILE_192x256 = 3,
+  QE_TILE_256x128 = 4
+} qe_gemm_tile;
+qe_status qe_set_gemm_tile(qe_gemm_tile tile);
+
 /* ------------------------------------------------------------------------
  * Stage context: layers, tape slots, versions, arena, executor
  * ------------------------------------------------------------------------ */

@@ -541,6 +541,12 @@ qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t row
   return QE_OK;
 }
 
+qe_status qe_set_gemm_tile(qe_gemm_tile tile) {
+  if (tile < QE_TILE_AUTO || tile > QE_TILE_256x128) return QE_ERR_INVALID_ARG;
+  qe::set_gemm_tile_override(int(tile));
+  return QE_OK;
+}
+
 qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const uint8_t *b, qe_fp8_fmt fmt_b,
                          int64_t ldb, int64_t m, int64_t n, int64_t k, const float *a_scale_inv,
                          const float *b_scale_inv, void *c, qe_dtype c_dtype, int64_t ldc, qe_place_mode mode,

@@ -50,6 +50,8 @@
 // same bits, which the split-vs-full-backward check relies on.
 #include "kernels.h"
 
+#include <atomic>
+
 namespace qe {
 namespace {
 
@@ -327,12 +329,19 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 // barrier sits between the two half-steps of a tile, so the first fragment
 // reads of the next tile overlap the second half-step's MFMAs; LDS-bound loads
 // run two tiles ahead of the MFMAs.
-template <int FA, int FB, int OUT>
+template <int FA, int FB, int OUT, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok) {
-  constexpr int BM = 256, BN = 256, NW = 4, TM = 128, TN = 128;
-  constexpr int CH = BM * (BK / 16) / 256;  // 16-byte chunks per lane per operand tile (8)
+  static_assert((BM == 256 || BM == 192) && (BN == 256 || BN == 192), "tile sizes");
+  constexpr int NW = 4, TM = BM / 2, TN = BN / 2;
+  constexpr int I = TM / 32, J = TN / 32;   // 32 x 32 MFMA blocks per wave sub-tile
+  constexpr int CHA = BM / 32, CHB = BN / 32;  // 16-byte LDS-bound loads per lane per K tile
+  constexpr int NQ = I * J;                  // MFMAs per half-step
+  constexpr int NR = I + J;                  // fragment reads per half-step
+  constexpr int ND = CHA + CHB;              // LDS-bound loads per K tile
   constexpr int STAGE = (BM + BN) * BK;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+  constexpr int EP = TN + 4;                 // epilogue staging row, in floats (padded)
+  constexpr int SMEM = 2 * STAGE > NW * 32 * EP * 4 ? 2 * STAGE : NW * 32 * EP * 4;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -354,12 +363,17 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   const int T = KT + (ktail > 0 ? 1 : 0);
 
   const int lrow = lane >> 3;
-  uint32_t oa[CH], ob[CH];
+  uint32_t oa[CHA], ob[CHB];
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
+  for (int c = 0; c < CHA; ++c) {
     const int row = 8 * (wave + NW * c) + lrow;
     const int lch = (lane & 7) ^ ((row >> 1) & 7);
     oa[c] = uint32_t(min(m0 + row, M - 1) * g.lda) + lch * 16;
+  }
+#pragma unroll
+  for (int c = 0; c < CHB; ++c) {
+    const int row = 8 * (wave + NW * c) + lrow;
+    const int lch = (lane & 7) ^ ((row >> 1) & 7);
     ob[c] = uint32_t(min(n0 + row, N - 1) * g.ldb) + lch * 16;
   }
   const uint32_t lds_base = uint32_t(reinterpret_cast<uintptr_t>(smem));
@@ -372,11 +386,11 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       const uint32_t sa = wblk + uint32_t(buf * STAGE);
       const uint32_t sb = sa + uint32_t(BM * BK);
 #pragma unroll
-      for (int c = 0; c < CH; ++c)
+      for (int c = 0; c < CHA; ++c)
         asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[c]), "s"(ga),
                      "s"(sa + uint32_t(c * NW * 1024)) : "memory", "m0");
 #pragma unroll
-      for (int c = 0; c < CH; ++c)
+      for (int c = 0; c < CHB; ++c)
         asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[c]), "s"(gb),
                      "s"(sb + uint32_t(c * NW * 1024)) : "memory", "m0");
     } else {  // the last, partial K tile, through registers: bytes at or past K are zero
@@ -384,12 +398,17 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       uint8_t *dB = dA + BM * BK;
       const uint32_t k0 = uint32_t(KT) * BK;
 #pragma unroll
-      for (int c = 0; c < CH; ++c) {
+      for (int c = 0; c < CHA; ++c) {
         const int row = 8 * (wave + NW * c) + lrow;
         const int64_t gk = int64_t(k0) + (((lane & 7) ^ ((row >> 1) & 7)) * 16);
         const uint4 va = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.a + (oa[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
-        const uint4 vb = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.b + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
         *reinterpret_cast<uint4 *>(dA + (wave + NW * c) * 1024 + lane * 16) = va;
+      }
+#pragma unroll
+      for (int c = 0; c < CHB; ++c) {
+        const int row = 8 * (wave + NW * c) + lrow;
+        const int64_t gk = int64_t(k0) + (((lane & 7) ^ ((row >> 1) & 7)) * 16);
+        const uint4 vb = gk < K ? mask_tail(*reinterpret_cast<const uint4 *>(g.b + (ob[c] + k0)), K - gk) : make_uint4(0u, 0u, 0u, 0u);
         *reinterpret_cast<uint4 *>(dB + (wave + NW * c) * 1024 + lane * 16) = vb;
       }
     }
@@ -410,61 +429,59 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
     const uint4 hi = *reinterpret_cast<const uint4 *>(base + fo[h][1]);
     return v8i{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
   };
-  auto load_frags = [&](int buf, int h, v8i (&fa)[4], v8i (&fb)[4]) {
+  auto load_frags = [&](int buf, int h, v8i (&fa)[I], v8i (&fb)[J]) {
     const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
     const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) fa[i] = frag(a_s + i * 32 * BK, h);
+    for (int i = 0; i < I; ++i) fa[i] = frag(a_s + i * 32 * BK, h);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = frag(b_s + j * 32 * BK, h);
+    for (int j = 0; j < J; ++j) fb[j] = frag(b_s + j * 32 * BK, h);
   };
 
-  v16f acc[4][4];
+  v16f acc[I][J];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < I; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < J; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  auto mfma_all = [&](const v8i (&fa)[4], const v8i (&fb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
-  };
 
   // One fragment read (or one LDS-bound load) is issued after each MFMA, in
   // this exact order (sched_barrier), so the single wave per SIMD keeps the
   // MFMA pipe busy while its memory instructions issue in the MFMA shadow.
-  auto read_one = [&](int buf, int h, int q, v8i (&fa)[4], v8i (&fb)[4]) {
-    // q = 0..7: a0, b0, b1, b2, b3, a1, a2, a3 (the order the MFMAs need them)
+  auto read_one = [&](int buf, int h, int q, v8i (&fa)[I], v8i (&fb)[J]) {
+    // q = 0 .. I+J-1: a0, b0 .. b(J-1), a1 .. a(I-1) (the order the MFMAs need them)
     const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
     const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
     if (q == 0) fa[0] = frag(a_s, h);
-    else if (q <= 4) fb[q - 1] = frag(b_s + (q - 1) * 32 * BK, h);
-    else fa[q - 4] = frag(a_s + (q - 4) * 32 * BK, h);
+    else if (q <= J) fb[q - 1] = frag(b_s + (q - 1) * 32 * BK, h);
+    else fa[q - J] = frag(a_s + (q - J) * 32 * BK, h);
   };
+  // the q-th of the ND LDS-bound loads of a K tile (q < CHA: A, else B)
   auto dma_one = [&](int kt, int buf, int q) {
     const uint32_t sa = wblk + uint32_t(buf * STAGE);
-    if (q < CH) {
+    if (q < CHA) {
       const uint8_t *ga = g.a + int64_t(kt) * BK;
       asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[q]), "s"(ga),
                    "s"(sa + uint32_t(q * NW * 1024)) : "memory", "m0");
     } else {
       const uint8_t *gb = g.b + int64_t(kt) * BK;
-      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[q - CH]), "s"(gb),
-                   "s"(sa + uint32_t(BM * BK) + uint32_t((q - CH) * NW * 1024)) : "memory", "m0");
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[q - CHA]), "s"(gb),
+                   "s"(sa + uint32_t(BM * BK) + uint32_t((q - CHA) * NW * 1024)) : "memory", "m0");
     }
   };
-  auto mfma_one = [&](int q, const v8i (&fa)[4], const v8i (&fb)[4]) {
-    const int i = q >> 2, j = q & 3;
+  // loads issued after the q-th MFMA of a half-step: [q ND / NQ, (q+1) ND / NQ)
+  auto dma_slot = [&](int kt, int buf, int q) {
+#pragma unroll
+    for (int d = q * ND / NQ; d < (q + 1) * ND / NQ; ++d) dma_one(kt, buf, d);
+  };
+  auto mfma_one = [&](int q, const v8i (&fa)[I], const v8i (&fb)[J]) {
+    const int i = q / J, j = q % J;
     acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
   };
 
   if (T > 0) {
-    v8i a0[4], b0[4], a1[4], b1[4];
+    v8i a0[I], b0[J], a1[I], b1[J];
     issue(0, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -472,11 +489,11 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
     if (T > 1) issue(1, 1);
     // first half of tile 0: MFMAs on set 0, reads of set 1 (tile 0, second half)
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       __builtin_amdgcn_sched_barrier(0);
       mfma_one(q, a0, b0);
       __builtin_amdgcn_sched_barrier(0);
-      if (q < 8) read_one(0, 1, q, a1, b1);
+      if (q < NR) read_one(0, 1, q, a1, b1);
     }
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -491,24 +508,24 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       if (t + 2 < T && !dma) issue(t + 2, buf);
       // second half of tile t: MFMAs on set 1, loads of tile t+2, reads of set 0 (tile t+1)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
+      for (int q = 0; q < NQ; ++q) {
         __builtin_amdgcn_sched_barrier(0);
         mfma_one(q, a1, b1);
         __builtin_amdgcn_sched_barrier(0);
-        if (dma) dma_one(t + 2, buf, q);
+        if (dma) dma_slot(t + 2, buf, q);
         // unconditional: in the last iteration this reads a stale stage that
         // is never used (always in bounds), and keeps the loop branch-free here
-        if (q >= 8) read_one(buf ^ 1, 0, q - 8, a0, b0);
+        if (q >= NQ - NR) read_one(buf ^ 1, 0, q - (NQ - NR), a0, b0);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (t + 1 < T) {
         // first half of tile t+1: MFMAs on set 0, reads of set 1 (tile t+1, second half)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
+        for (int q = 0; q < NQ; ++q) {
           __builtin_amdgcn_sched_barrier(0);
           mfma_one(q, a0, b0);
           __builtin_amdgcn_sched_barrier(0);
-          if (q < 8) read_one(buf ^ 1, 1, q, a1, b1);
+          if (q < NR) read_one(buf ^ 1, 1, q, a1, b1);
         }
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -523,7 +540,6 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   // rows padded to 132 floats) into LDS, then reads it back row-contiguous:
   // 32 lanes x 16 B cover one 512-byte output row run per store instruction.
   __syncthreads();  // every wave is done reading the last stage
-  constexpr int EP = 132;  // padded row, in floats
   float *ep = reinterpret_cast<float *>(smem) + wave * 32 * EP;
   const int e = pow2_exponent(g.a_scale_inv) + pow2_exponent(g.b_scale_inv);
   const bool nfull = n0 + BN <= N;
@@ -536,6 +552,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   // (buffer instructions: the row offset is a scalar operand; every offset of
   // the wave's 128 x 128 block stays below 2^31)
   const bool fast = vec_ok && nfull && m0 + BM <= M && g.ldc * ES * (TM + 2) < (int64_t(1) << 31);
+  const bool has_col = (lane & 31) * 4 < TN;  // TN = 96: 24 of each 32 lanes hold a column quad
   const int wu = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t voff = uint32_t((lane >> 5) * g.ldc + (lane & 31) * 4) * uint32_t(ES);
   char *cbase = static_cast<char *>(g.c) + ((m0 + (wu >> 1) * TM) * g.ldc + n0 + (wu & 1) * TN) * ES;
@@ -544,7 +561,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   float *ew = ep + (lane & 31) * EP + 4 * (lane >> 5);
   const float *er = ep + (lane >> 5) * EP + (lane & 31) * 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < I; ++i) {
     // accumulate: read this block's destination first, so the loads are in
     // flight during the LDS round trip instead of one dependent load per row
     float4 pre[16];
@@ -552,20 +569,20 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       if (fast) {
 #pragma unroll
         for (int it = 0; it < 16; ++it)
-          pre[it] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, (i * 32 + 2 * it) * rstep, 0));
+          if (has_col) pre[it] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, (i * 32 + 2 * it) * rstep, 0));
       } else {
 #pragma unroll
         for (int it = 0; it < 16; ++it) {
           const int64_t row = m0 + wm * TM + i * 32 + 2 * it + (lane >> 5);
           const int64_t col = n0 + wn * TN + (lane & 31) * 4;
           pre[it] = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (row < M && vec_ok && (nfull || col + 4 <= N))
+          if (has_col && row < M && vec_ok && (nfull || col + 4 <= N))
             pre[it] = *reinterpret_cast<const float4 *>(static_cast<const float *>(g.c) + row * g.ldc + col);
         }
       }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < J; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         *reinterpret_cast<float4 *>(ew + j * 32 + 8 * q) =
@@ -576,6 +593,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
     if (fast) {
 #pragma unroll
       for (int it = 0; it < 16; ++it) {
+        if (!has_col) continue;
         const float4 v4 = *reinterpret_cast<const float4 *>(er + it * 2 * EP);
         const int so = (i * 32 + 2 * it) * rstep;
         if constexpr (OUT == 0) {
@@ -597,6 +615,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       const int64_t row = m0 + wm * TM + i * 32 + r;
       const int cl = (lane & 31) * 4;
       const int64_t col = n0 + wn * TN + cl;
+      if (!has_col) continue;
       const float4 v4 = *reinterpret_cast<const float4 *>(ep + r * EP + cl);
       if (row >= M) continue;
       const float v[4] = {v4.x, v4.y, v4.z, v4.w};
@@ -630,25 +649,26 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   }
 }
 
-template <int FA, int FB>
+template <int FA, int FB, int BM, int BN>
 hipError_t launch_w4(const GemmParams &g, hipStream_t s) {
-  const int tiles_m = int((g.m + 255) / 256), tiles_n = int((g.n + 255) / 256);
+  const int tiles_m = int((g.m + BM - 1) / BM), tiles_n = int((g.n + BN - 1) / BN);
   const uintptr_t cp = reinterpret_cast<uintptr_t>(g.c);
   const int vec_ok = (g.out == 1) ? (g.ldc % 4 == 0 && cp % 8 == 0) : (g.ldc % 4 == 0 && cp % 16 == 0);
   const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n)), block(256);
   switch (g.out) {
-    case 0: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 0>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    case 1: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 1>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    default: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 2>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    case 0: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 0, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    case 1: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 1, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    default: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 2, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
   }
   return hipGetLastError();
 }
 
+template <int BM, int BN>
 hipError_t launch_w4_fmts(const GemmParams &g, hipStream_t s) {
-  if (g.fmt_a == 0 && g.fmt_b == 0) return launch_w4<0, 0>(g, s);
-  if (g.fmt_a == 1 && g.fmt_b == 0) return launch_w4<1, 0>(g, s);
-  if (g.fmt_a == 0 && g.fmt_b == 1) return launch_w4<0, 1>(g, s);
-  return launch_w4<1, 1>(g, s);
+  if (g.fmt_a == 0 && g.fmt_b == 0) return launch_w4<0, 0, BM, BN>(g, s);
+  if (g.fmt_a == 1 && g.fmt_b == 0) return launch_w4<1, 0, BM, BN>(g, s);
+  if (g.fmt_a == 0 && g.fmt_b == 1) return launch_w4<0, 1, BM, BN>(g, s);
+  return launch_w4<1, 1, BM, BN>(g, s);
 }
 
 template <int BM, int BN, int WM, int WN, int FA, int FB>
@@ -674,6 +694,15 @@ hipError_t launch_fmts(const GemmParams &g, hipStream_t s) {
 }
 
 }  // namespace
+
+// Relative cost of a round of tiles against a round of 256 x 256 ones at the
+// same K, measured on MI355X (K = 4096): 256 x 192 or 192 x 256 ~0.76 (0.75
+// of the MFMA work at a slightly lower efficiency per FLOP), the 8-wave
+// 256 x 128 kernel ~0.68.  Rounded up, so a tie keeps the larger tile.
+constexpr double kCost192 = 0.80;
+constexpr double kCost128 = 0.70;
+
+static std::atomic<int> g_tile_override{0};
 
 hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
@@ -706,16 +735,33 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
     return hipSuccess;
   }
   // Tile choice by wave quantization: each CU runs one workgroup at a time, so
-  // a grid costs ceil(tiles / CUs) rounds of one tile's time.  A round of the
-  // 256 x 128 kernel takes ~0.62 of a round of the 256 x 256 one (measured on
-  // MI355X; it is less efficient per FLOP), so it wins when the 256 x 256 grid
-  // leaves the last round mostly empty (e.g. N = 6144: 384 tiles).
-  const int64_t t256 = ((g.m + 255) / 256) * ((g.n + 255) / 256);
-  const int64_t t128 = ((g.m + 255) / 256) * ((g.n + 127) / 128);
-  const double c256 = double((t256 + kCUs - 1) / kCUs);
-  const double c128 = 0.62 * double((t128 + kCUs - 1) / kCUs);
-  if (c128 < c256) return launch_fmts<256, 128, 4, 2>(g, s);
-  return launch_w4_fmts(g, s);
+  // a grid costs ceil(tiles / CUs) rounds of one tile's time; the smaller tiles
+  // win where the 256 x 256 grid leaves its last round mostly empty (N = 6144:
+  // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.76).
+  auto rounds = [&](int64_t bm, int64_t bn) {
+    const int64_t t = ((g.m + bm - 1) / bm) * ((g.n + bn - 1) / bn);
+    return double((t + kCUs - 1) / kCUs);
+  };
+  const int force = g_tile_override.load(std::memory_order_relaxed);
+  const double c256 = rounds(256, 256);
+  const double c128 = kCost128 * rounds(256, 128);
+  const double cn192 = kCost192 * rounds(256, 192);
+  const double cm192 = kCost192 * rounds(192, 256);
+  if (force == 1) return launch_w4_fmts<256, 256>(g, s);
+  if (force == 2) return launch_w4_fmts<256, 192>(g, s);
+  if (force == 3) return launch_w4_fmts<192, 256>(g, s);
+  if (force == 4) return launch_fmts<256, 128, 4, 2>(g, s);
+  double best = c256;
+  int pick = 1;
+  if (cn192 < best) { best = cn192; pick = 2; }
+  if (cm192 < best) { best = cm192; pick = 3; }
+  if (c128 < best) { best = c128; pick = 4; }
+  if (pick == 2) return launch_w4_fmts<256, 192>(g, s);
+  if (pick == 3) return launch_w4_fmts<192, 256>(g, s);
+  if (pick == 4) return launch_fmts<256, 128, 4, 2>(g, s);
+  return launch_w4_fmts<256, 256>(g, s);
 }
+
+void set_gemm_tile_override(int tile) { g_tile_override.store(tile, std::memory_order_relaxed); }
 
 }  // namespace qe

@@ -101,6 +101,8 @@ enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COPY = 3, KC_AMA
 hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s);
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
+// 0: tile shape from the cost model; 1..4: force 256x256, 256x192, 192x256, 256x128
+void set_gemm_tile_override(int tile);
 hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s);
 hipError_t launch_amax(const AmaxParams &p, hipStream_t s);
 AmaxParams amax_params(const void *in, bool bf16, int64_t numel, float *amax, float *accum);

@@ -86,6 +86,7 @@ _SIGS = {
     "qe_amax": [_P, _I32, _I64, C.POINTER(FP8Meta), _P],
     "qe_quantize_fp8_current": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P, _P],
     "qe_fp8_gemm_tn": [_P, _I32, _I64, _P, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _I32, _I64, _I32, _P],
+    "qe_set_gemm_tile": [_I32],
     "qe_ctx_create": [C.POINTER(Config), C.POINTER(_P)],
     "qe_layer_register": [_P, C.POINTER(LayerDesc), C.POINTER(_I32)],
     "qe_layer_meta": [_P, _I32, _I32, C.POINTER(FP8Meta)],
@@ -194,6 +195,13 @@ def qe_fp8_gemm_tn(a, fmt_a: int, lda: int, b, fmt_b: int, ldb: int, m: int, n: 
                    b_scale_inv, c, c_dtype: int, ldc: int, mode: int = INIT, stream=None) -> str:
     return _st(lib().qe_fp8_gemm_tn(ptr(a), fmt_a, lda, ptr(b), fmt_b, ldb, m, n, k, ptr(a_scale_inv),
                                     ptr(b_scale_inv), ptr(c), c_dtype, ldc, mode, stream_handle(stream)))
+
+
+TILE_AUTO, TILE_256x256, TILE_256x192, TILE_192x256, TILE_256x128 = 0, 1, 2, 3, 4
+
+
+def qe_set_gemm_tile(tile: int) -> str:
+    return _st(lib().qe_set_gemm_tile(tile))
 
 
 def make_meta(hist, scale, scale_inv, fmt: int, margin: int = 0, amax_accum=None) -> FP8Meta:

@@ -161,3 +161,81 @@ def test_large_grids_bit_exact(shape):
     assert qe.qe_fp8_gemm_tn(a_t, 0, k, b_t, 0, k, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
     ref = (ai.double() @ bi.double().T).float()
     assert torch.equal(c, ref)
+
+
+@pytest.fixture
+def forced_tile():
+    """Sets a forced macro-tile shape for one test and restores the cost model after it."""
+    qe = need_lib()
+    yield qe
+    assert qe.qe_set_gemm_tile(qe.TILE_AUTO) == "OK"
+
+
+def _int_operands(d, m, n, k, seed):
+    """Integer-valued E4M3 operands with rows padded to a multiple of 16 bytes
+    (padding codes are arbitrary and must be ignored)."""
+    g = torch.Generator(device=d)
+    g.manual_seed(seed)
+    ld = rup16(k)
+    ai = torch.randint(-6, 7, (m, ld), device=d, generator=g)
+    bi = torch.randint(-6, 7, (n, ld), device=d, generator=g)
+    lut = torch.from_numpy(fp8.encode(np.arange(-6, 7, dtype=np.float64), "E4M3")).to(d)
+    return ai[:, :k], bi[:, :k], lut[(ai + 6)].contiguous(), lut[(bi + 6)].contiguous()
+
+
+# full tiles of every shape, ragged edges in M, N and K, a partial last K tile,
+# and grids of several rounds
+TILE_SHAPES = [(768, 768, 256), (1000, 700, 320), (576, 4096, 384), (4096, 576, 130), (2304, 2304, 512),
+               (193, 191, 129), (4096, 6144, 256)]
+
+
+@pytest.mark.parametrize("tile", [1, 2, 3, 4], ids=["256x256", "256x192", "192x256", "256x128"])
+@pytest.mark.parametrize("shape", TILE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_forced_tile_shapes_exact(forced_tile, tile, shape):
+    """Each macro-tile shape on integer operands: FP32 store, BF16 store and
+    FP32 accumulate into a strided view are exact (every partial sum is an
+    integer below 2^24), on full tiles (the branch-free epilogue) and on ragged
+    edges (the checked one)."""
+    qe = forced_tile
+    d = dev()
+    assert qe.qe_set_gemm_tile(tile) == "OK"
+    m, n, k = shape
+    ai, bi, a_t, b_t = _int_operands(d, m, n, k, 5 + tile)
+    lda = a_t.shape[1]
+    ref = ai.double() @ bi.double().T
+    s = torch.tensor([1.0, 1.0], dtype=torch.float32, device=d)
+    c = torch.empty((m, n), dtype=torch.float32, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+    assert torch.equal(c, ref.float())
+    # bf16: the exact FP32 result rounded to nearest even
+    cb = torch.empty((m, n), dtype=torch.int16, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], cb, qe.BF16, n) == "OK"
+    assert torch.equal(cb.view(torch.bfloat16), ref.float().to(torch.bfloat16))
+    # accumulate into a view with ld > n; the padding columns stay untouched
+    ld = n + 8
+    base = torch.randint(-50, 50, (m, ld), device=d, generator=torch.Generator(device=d).manual_seed(3)).float()
+    ca = base.clone()
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], ca, qe.F32, ld, qe.ACCUM) == "OK"
+    torch.cuda.synchronize()
+    assert torch.equal(ca[:, :n], (base[:, :n].double() + ref).float())
+    assert torch.equal(ca[:, n:], base[:, n:])
+
+
+@pytest.mark.parametrize("shape", [(768, 768, 1000), (1000, 700, 320), (576, 4096, 384)], ids=str)
+def test_four_wave_tile_shapes_same_bits(forced_tile, shape):
+    """256x256, 256x192 and 192x256 run the same MFMA in the same K order: on
+    random codes (inexact FP32 sums) their outputs are bit-identical."""
+    qe = forced_tile
+    d = dev()
+    m, n, k = shape
+    rng = np.random.default_rng(m + n + k)
+    A = random_codes(rng, m, k, 0, rup16(k))
+    B = random_codes(rng, n, k, 1, rup16(k))
+    outs = []
+    for tile in (1, 2, 3):
+        assert qe.qe_set_gemm_tile(tile) == "OK"
+        outs.append(run_gemm(qe, d, A, 0, B, 1, m, n, k, 2.0 ** -2, 2.0 ** 3, qe.F32, n)[: m * n])
+    ref = gemm.gemm_tn(A[:, :k], "E4M3", B[:, :k], "E5M2", 2.0 ** -2, 2.0 ** 3)
+    assert rel_err(outs[0].reshape(m, n), ref) <= 1e-3
+    np.testing.assert_array_equal(outs[1], outs[0])
+    np.testing.assert_array_equal(outs[2], outs[0])
