@@ -188,9 +188,8 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
  * measured per-round cost; the others force one shape (for tests and
  * measurements).  Process-wide; it applies to launches enqueued afterwards
  * (a graph captured earlier keeps the shapes it was captured with).  The
- * three 4-wave shapes (256x256, 256x192, 192x256) give the same bits: the same
- * 32x32x64 MFMA and the same order along K, no split reduction.  256x128 uses
- * the 16x16x128 MFMA and may differ from them in the last bits.
+ * four shapes give the same bits: the same 16x16x128 MFMA with the same
+ * reduction bytes per lane, the same order along K, no split reduction.
  * Errors: QE_ERR_INVALID_ARG for a value outside the enum. */
 typedef enum {
   QE_TILE_AUTO = 0,

@@ -10,27 +10,29 @@
 // it to an FP32 destination in place: the direct placement of dW into its
 // slice of the flat main-gradient buffer (§3.4), with no staging copy.
 //
-// Two kernels share the scheme below.
-//  * gemm_tn_w4_kernel, 256 x 256 x 128 tiles: four waves (one per SIMD) on a
-//    2 x 2 grid, each a 128 x 128 sub-tile of 4 x 4 v_mfma_f32_32x32x64_f8f6f4
-//    blocks.  A K tile is two 64-wide half-steps; one register set of
-//    fragments feeds 16 MFMAs while the other set is read from LDS, and every
-//    fragment read or LDS-bound load is issued right after an MFMA, in a fixed
-//    order (sched_barrier), so the MFMA pipe stays busy in the single wave.
-//    The K loop is rotated (second half-step of tile t, then first half-step
-//    of tile t+1) so that its back-edge sits at the stage barrier, where all
-//    LDS reads have completed; the compiler can then wait for fragment reads
-//    one by one instead of draining them at the loop head.  The epilogue goes
-//    through LDS so every store instruction writes whole 512-byte row runs.
-//    Larger wave tiles mean less LDS traffic per FLOP than eight waves.
+// Two kernels share the scheme below; both use v_mfma_f32_16x16x128_f8f6f4
+// with the same assignment of reduction bytes to lanes, so every tile shape
+// accumulates each output element in the same order and gives the same bits.
+//  * gemm_tn_w4_kernel, 256 x 256 x 128 tiles (and 256 x 192, 192 x 256):
+//    four waves (one per SIMD) on a 2 x 2 grid, each a 128 x 128 sub-tile of
+//    8 x 8 MFMA blocks.  A K tile's 64 MFMAs run in two phases; every fragment
+//    read or LDS-bound load is issued right after an MFMA, in a fixed order
+//    (sched_barrier), so the MFMA pipe stays busy in the single wave, and the
+//    LDS-bound loads are branch-free (two instructions each) because a single
+//    wave issues at most one instruction per four cycles, eight per MFMA.
+//    The K loop is rotated so that its back-edge sits at the stage barrier,
+//    where all LDS reads have completed; the compiler can then wait for
+//    fragment reads one by one instead of draining them at the loop head.
+//    The epilogue goes through LDS so every store instruction writes whole
+//    512-byte row runs.  Larger wave tiles mean less LDS traffic per FLOP
+//    than eight waves.
 //  * gemm_tn_kernel, 256 x 128 x 128 tiles: eight waves (two per SIMD) on a
-//    4 x 2 grid with v_mfma_f32_16x16x128_f8f6f4; used when it quantizes better
-//    onto the 256 CUs.
+//    4 x 2 grid; used when it quantizes better onto the 256 CUs.
 // Operand formats (E4M3 or E5M2) are chosen per call.  K tiles are
 // double-buffered in LDS and filled by LDS-bound global loads
 // (global_load_lds_dwordx4: no register staging, no LDS store instructions)
-// issued a K tile ahead; each wave waits for its own loads and a barrier
-// publishes the stage.  LDS rows are 128 bytes; their 16-byte chunks are
+// issued a K tile ahead (the 4-wave kernel: a K tile and a phase); each wave
+// waits for its own loads and a barrier publishes the stage.  LDS rows are 128 bytes; their 16-byte chunks are
 // XOR-swizzled by (row/2) mod 8 so a fragment read hits the 64 banks evenly,
 // and since fragments start on multiples of 16 rows, every fragment of a wave
 // is one base address plus a constant.  The LDS-bound loads are inline
@@ -329,28 +331,43 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   }
 }
 
-typedef float v16f __attribute__((ext_vector_type(16)));
-
-// 256 x 256 x 128 tile, four waves (one per SIMD) on a 2 x 2 grid, each wave a
-// 128 x 128 sub-tile of 4 x 4 v_mfma_f32_32x32x64_f8f6f4 blocks.  A K tile is
-// two 64-wide half-steps; the fragments of the next half-step are read into a
-// second register set while the 16 MFMAs of the current one run.  The stage
-// barrier sits between the two half-steps of a tile, so the first fragment
-// reads of the next tile overlap the second half-step's MFMAs; LDS-bound loads
-// run two tiles ahead of the MFMAs.
+// 256 x 256 x 128 tile (also 256 x 192 and 192 x 256), four waves (one per
+// SIMD) on a 2 x 2 grid, each wave a TM x TN sub-tile of 16 x 16 blocks of
+// v_mfma_f32_16x16x128_f8f6f4, one MFMA per block per K tile.  (On random FP8
+// operands this MFMA sustains about a third more throughput than the 32 x 32 x
+// 64 one on MI355X, which draws more power per FLOP; with constant operands
+// the two are equal.)
+// A K tile's MFMAs run in two phases of I/2 block rows each:
+//   phase A (block rows 0 .. I/2-1, column-major): uses A fragments
+//     0 .. I/2-1 and every B fragment; reads A fragments I/2 .. I-1 of the
+//     same tile;
+//   phase B (block rows I/2 .. I-1, column-major): each B fragment's last use
+//     is followed by the read of the next tile's B fragment into the same
+//     registers, and the next tile's A fragments 0 .. I/2-1 are read too; the
+//     LDS-bound loads of the tile after next are issued.
+// So all of tile t is read by the end of its phase A, where the stage barrier
+// sits: it frees tile t's stage for the loads of tile t+2 and publishes tile
+// t+1, whose loads were issued during the previous phase B (one K tile of
+// latency budget).  Fragment registers: I + J fragments of 8 VGPRs, no second
+// set.  The K loop is rotated (phase B of tile t, then phase A of tile t+1)
+// so its back-edge sits at the barrier, where every LDS read has completed;
+// the waits for fragment reads inside an iteration can then be partial.
 template <int FA, int FB, int OUT, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok) {
   static_assert((BM == 256 || BM == 192) && (BN == 256 || BN == 192), "tile sizes");
   constexpr int NW = 4, TM = BM / 2, TN = BN / 2;
-  constexpr int I = TM / 32, J = TN / 32;   // 32 x 32 MFMA blocks per wave sub-tile
+  constexpr int I = TM / 16, J = TN / 16;    // 16 x 16 MFMA blocks per wave sub-tile
+  constexpr int IA = I / 2, IB = I - IA;     // block rows of phase A and phase B
+  constexpr int QA = IA * J, QB = IB * J;    // MFMAs per phase
   constexpr int CHA = BM / 32, CHB = BN / 32;  // 16-byte LDS-bound loads per lane per K tile
-  constexpr int NQ = I * J;                  // MFMAs per half-step
-  constexpr int NR = I + J;                  // fragment reads per half-step
   constexpr int ND = CHA + CHB;              // LDS-bound loads per K tile
   constexpr int STAGE = (BM + BN) * BK;
   constexpr int EP = TN + 4;                 // epilogue staging row, in floats (padded)
-  constexpr int SMEM = 2 * STAGE > NW * 32 * EP * 4 ? 2 * STAGE : NW * 32 * EP * 4;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
+  static_assert(NW * 32 * EP * 4 <= 2 * STAGE, "epilogue staging fits in the stages");
+  static_assert(CHA * NW * 1024 == BM * BK, "LDS-bound load d of a tile lands at stage + 4096 d");
+  // two K stages, then one 1 KB block per wave that absorbs the loads issued
+  // past the last full K tile (so the loop issues them unconditionally)
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE + NW * 1024];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -387,6 +404,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   }
   const uint32_t lds_base = uint32_t(reinterpret_cast<uintptr_t>(smem));
   const uint32_t wblk = __builtin_amdgcn_readfirstlane(lds_base + uint32_t(wave) * 1024u);
+  const uint32_t wdummy = __builtin_amdgcn_readfirstlane(lds_base + uint32_t(2 * STAGE) + uint32_t(wave) * 1024u);
 
   auto issue = [&](int kt, int buf) {
     if (kt < KT) {
@@ -423,74 +441,96 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
     }
   };
 
-  // 32-row fragments: lane l reads row (l & 31), the 32 bytes 32 (l >> 5) .. +31
-  // of the 64-wide half-step h, i.e. chunks 4h + 2 (l >> 5) and the next.  The
-  // swizzle term depends on (l & 31) only, so fragments are base + constant.
-  const int fr = lane & 31, fh = lane >> 5;
-  uint32_t fo[2][2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    fo[h][0] = uint32_t(fr) * BK + (uint32_t((4 * h + 2 * fh) ^ (fr >> 1)) & 7) * 16;
-    fo[h][1] = uint32_t(fr) * BK + (uint32_t((4 * h + 2 * fh + 1) ^ (fr >> 1)) & 7) * 16;
-  }
-  auto frag = [&](const uint8_t *base, int h) -> v8i {
-    const uint4 lo = *reinterpret_cast<const uint4 *>(base + fo[h][0]);
-    const uint4 hi = *reinterpret_cast<const uint4 *>(base + fo[h][1]);
+  // 16-row fragments: lane l reads row (l & 15), the 32 bytes 32 (l >> 4) .. +31
+  // of the K tile, i.e. logical chunks 2 (l >> 4) and the next.  The swizzle
+  // term depends on (l & 15) only, so every fragment is base + constant.
+  const int fr = lane & 15, fq = lane >> 4;
+  const uint32_t f_lo = uint32_t(fr) * BK + (uint32_t((2 * fq) ^ (fr >> 1)) & 7) * 16;
+  const uint32_t f_hi = uint32_t(fr) * BK + (uint32_t((2 * fq + 1) ^ (fr >> 1)) & 7) * 16;
+  auto frag = [&](const uint8_t *base) -> v8i {
+    const uint4 lo = *reinterpret_cast<const uint4 *>(base + f_lo);
+    const uint4 hi = *reinterpret_cast<const uint4 *>(base + f_hi);
     return v8i{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
   };
-  auto load_frags = [&](int buf, int h, v8i (&fa)[I], v8i (&fb)[J]) {
-    const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
-    const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
-#pragma unroll
-    for (int i = 0; i < I; ++i) fa[i] = frag(a_s + i * 32 * BK, h);
-#pragma unroll
-    for (int j = 0; j < J; ++j) fb[j] = frag(b_s + j * 32 * BK, h);
+  auto read_a = [&](int buf, int i, v8i (&fa)[I]) { fa[i] = frag(smem + buf * STAGE + (wm * TM + i * 16) * BK); };
+  auto read_b = [&](int buf, int j, v8i (&fb)[J]) {
+    fb[j] = frag(smem + buf * STAGE + (BM + wn * TN + j * 16) * BK);
   };
 
-  v16f acc[I][J];
+  v4f acc[I][J];
 #pragma unroll
   for (int i = 0; i < I; ++i)
 #pragma unroll
-    for (int j = 0; j < J; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    for (int j = 0; j < J; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  // One fragment read (or one LDS-bound load) is issued after each MFMA, in
-  // this exact order (sched_barrier), so the single wave per SIMD keeps the
-  // MFMA pipe busy while its memory instructions issue in the MFMA shadow.
-  auto read_one = [&](int buf, int h, int q, v8i (&fa)[I], v8i (&fb)[J]) {
-    // q = 0 .. I+J-1: a0, b0 .. b(J-1), a1 .. a(I-1) (the order the MFMAs need them)
-    const uint8_t *a_s = smem + buf * STAGE + wm * TM * BK;
-    const uint8_t *b_s = smem + buf * STAGE + BM * BK + wn * TN * BK;
-    if (q == 0) fa[0] = frag(a_s, h);
-    else if (q <= J) fb[q - 1] = frag(b_s + (q - 1) * 32 * BK, h);
-    else fa[q - J] = frag(a_s + (q - J) * 32 * BK, h);
+  auto mfma = [&](int i, int j, const v8i (&fa)[I], const v8i (&fb)[J]) {
+    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
   };
-  // the q-th of the ND LDS-bound loads of a K tile (q < CHA: A, else B)
-  auto dma_one = [&](int kt, int buf, int q) {
-    const uint32_t sa = wblk + uint32_t(buf * STAGE);
-    if (q < CHA) {
-      const uint8_t *ga = g.a + int64_t(kt) * BK;
-      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(oa[q]), "s"(ga),
-                   "s"(sa + uint32_t(q * NW * 1024)) : "memory", "m0");
-    } else {
-      const uint8_t *gb = g.b + int64_t(kt) * BK;
-      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(ob[q - CHA]), "s"(gb),
-                   "s"(sa + uint32_t(BM * BK) + uint32_t((q - CHA) * NW * 1024)) : "memory", "m0");
-    }
+  // LDS-bound loads inside the K loop, two instructions each: load d of a K
+  // tile lands at stage + 4096 d, so M0 steps by a uniform stride, and the
+  // step is issued before an MFMA and the load after it (the MFMA is the wait
+  // state M0 needs).  Past the last full K tile the loads still run, from
+  // tile 0 into the wave's dummy block with stride 0: no branch per load.
+  auto dma_m0 = [&](int d, uint32_t base, uint32_t stride) {
+    if (d == 0)
+      asm volatile("s_mov_b32 m0, %0" ::"s"(base) : "m0");
+    else
+      asm volatile("s_add_u32 m0, m0, %0" ::"s"(stride) : "m0", "scc");
   };
-  // loads issued after the q-th MFMA of a half-step: [q ND / NQ, (q+1) ND / NQ)
-  auto dma_slot = [&](int kt, int buf, int q) {
+  auto dma_load = [&](int d, const uint8_t *ga, const uint8_t *gb) {
+    if (d < CHA)
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(oa[d]), "s"(ga) : "memory");
+    else
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(ob[d - CHA]), "s"(gb) : "memory");
+  };
+
+  // Phase A of a tile from stage `buf`: column-major MFMAs over block rows
+  // 0 .. IA-1 (B fragment j is first needed at MFMA j * IA, so the fragments
+  // read last in the previous phase B are needed last); A fragments IA .. I-1
+  // of the same tile are read after the first MFMAs (one per even slot), long
+  // before phase B needs them.
+  auto phase_a = [&](int buf, v8i (&fa)[I], v8i (&fb)[J]) {
 #pragma unroll
-    for (int d = q * ND / NQ; d < (q + 1) * ND / NQ; ++d) dma_one(kt, buf, d);
+    for (int q = 0; q < QA; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      mfma(q % IA, q / IA, fa, fb);
+      __builtin_amdgcn_sched_barrier(0);
+      if (q % 2 == 0 && q / 2 < IB) read_a(buf, IA + q / 2, fa);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   };
-  auto mfma_one = [&](int q, const v8i (&fa)[I], const v8i (&fb)[J]) {
-    const int i = q / J, j = q % J;
-    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], FB, FA, 0, 0, 0, 0);
+  // Phase B of a tile: column-major MFMAs over block rows IA .. I-1.  After
+  // the last use of B fragment j, the next tile's B fragment j is read from
+  // stage `nbuf` into the same registers; the next tile's A fragments
+  // 0 .. IA-1 are read in the first slots (their registers are free since
+  // phase A).  `dma` issues the loads of tile `kt2` into stage `buf`, spread
+  // evenly over the phase.
+  auto phase_b = [&](int nbuf, bool dma, int kt2, int buf, v8i (&fa)[I], v8i (&fb)[J]) {
+    static_assert(ND <= QB, "at most one LDS-bound load per MFMA");
+    const uint8_t *ga = dma ? g.a + int64_t(kt2) * BK : g.a;
+    const uint8_t *gb = dma ? g.b + int64_t(kt2) * BK : g.b;
+    const uint32_t base = dma ? wblk + uint32_t(buf * STAGE) : wdummy;
+    const uint32_t stride = dma ? uint32_t(NW * 1024) : 0u;
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      const int j = q / IB, i = IA + q % IB;
+      // load d follows MFMA q when d = floor(q ND / QB) steps up here
+      const bool ld = (q + 1) * ND / QB > q * ND / QB;
+      const int d = q * ND / QB;
+      __builtin_amdgcn_sched_barrier(0);
+      if (ld) dma_m0(d, base, stride);
+      __builtin_amdgcn_sched_barrier(0);  // M0 is written before the MFMA, never next to the load
+      mfma(i, j, fa, fb);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ld) dma_load(d, ga, gb);
+      if (q % 2 == 0 && q / 2 < IA) read_a(nbuf, q / 2, fa);
+      if (q % IB == IB - 1) read_b(nbuf, j, fb);  // last use of B fragment j was this MFMA
+    }
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   if (T > 0) {
-    v8i a0[I], b0[J], a1[I], b1[J];
+    v8i fa[I], fb[J];
     issue(0, 0);
     if (KT > 1) {
       // both first K tiles are full: tile 1's LDS-bound loads stay in flight
@@ -502,59 +542,33 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
     __syncthreads();
-    load_frags(0, 0, a0, b0);
-    if (T > 1 && KT <= 1) issue(1, 1);  // tile 1 is the partial tail: through registers
-    // first half of tile 0: MFMAs on set 0, reads of set 1 (tile 0, second half)
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_one(q, a0, b0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (q < NR) read_one(0, 1, q, a1, b1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    for (int j = 0; j < J; ++j) read_b(0, j, fb);
+#pragma unroll
+    for (int i = 0; i < IA; ++i) read_a(0, i, fa);
+    if (T > 1 && KT <= 1) issue(1, 1);  // tile 1 is the partial tail: through registers
+    phase_a(0, fa, fb);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();                       // tile 1 published; tile 0 fully read
-    // The loop is rotated so that its back-edge sits at the barrier, where every
-    // LDS read has completed anyway: the fragment reads of set 0 and their uses
-    // in the next half-step stay inside one iteration, and the waits for them
-    // can be partial instead of the full wait a loop header would need.
     for (int t = 0; t < T; ++t) {
       const int buf = t & 1;
       const bool dma = t + 2 < KT;
       if (t + 2 < T && !dma) issue(t + 2, buf);
-      // second half of tile t: MFMAs on set 1, loads of tile t+2, reads of set 0 (tile t+1)
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_one(q, a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
-        if (dma) dma_slot(t + 2, buf, q);
-        // unconditional: in the last iteration this reads a stale stage that
-        // is never used (always in bounds), and keeps the loop branch-free here
-        if (q >= NQ - NR) read_one(buf ^ 1, 0, q - (NQ - NR), a0, b0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+      // phase B of tile t; reads of tile t+1 (in the last iteration they read a
+      // stale stage that is never used: always in bounds, and branch-free here)
+      phase_b(buf ^ 1, dma, t + 2, buf, fa, fb);
       if (t + 1 < T) {
-        // first half of tile t+1: MFMAs on set 0, reads of set 1 (tile t+1, second half)
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          __builtin_amdgcn_sched_barrier(0);
-          mfma_one(q, a0, b0);
-          __builtin_amdgcn_sched_barrier(0);
-          if (q < NR) read_one(buf ^ 1, 1, q, a1, b1);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        phase_a(buf ^ 1, fa, fb);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();                   // tile t+2 published; tile t+1 fully read
       }
     }
   }
 
-  // Epilogue through LDS: the 32 x 32 MFMA layout gives each lane one row and
-  // scattered column quads, so store instructions would touch 32 rows x 32 B.
-  // Each wave instead writes one 32-row block of its sub-tile (32 x 128 FP32,
-  // rows padded to 132 floats) into LDS, then reads it back row-contiguous:
+  // Epilogue through LDS: the MFMA layout gives each lane one row and a column
+  // quad per 16 x 16 block, so store instructions would touch 16 rows x 64 B.
+  // Each wave instead writes one 32-row block of its sub-tile (32 x TN FP32,
+  // rows padded to TN + 4 floats) into LDS, then reads it back row-contiguous:
   // 32 lanes x 16 B cover one 512-byte output row run per store instruction.
   __syncthreads();  // every wave is done reading the last stage
   float *ep = reinterpret_cast<float *>(smem) + wave * 32 * EP;
@@ -567,7 +581,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   // instruction count is its time.  Other tiles take the checked path.
   constexpr int ES = OUT == 1 ? 2 : 4;  // output element bytes
   // (buffer instructions: the row offset is a scalar operand; every offset of
-  // the wave's 128 x 128 block stays below 2^31)
+  // the wave's TM x TN block stays below 2^31)
   const bool fast = vec_ok && nfull && m0 + BM <= M && g.ldc * ES * (TM + 2) < (int64_t(1) << 31);
   const bool has_col = (lane & 31) * 4 < TN;  // TN = 96: 24 of each 32 lanes hold a column quad
   const int wu = __builtin_amdgcn_readfirstlane(wave);
@@ -575,10 +589,10 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   char *cbase = static_cast<char *>(g.c) + ((m0 + (wu >> 1) * TM) * g.ldc + n0 + (wu & 1) * TN) * ES;
   const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(cbase, short(0), 0x7fffffff, 0x00020000);
   const int rstep = int(g.ldc) * ES;  // bytes per output row
-  float *ew = ep + (lane & 31) * EP + 4 * (lane >> 5);
+  float *ew = ep + (lane & 15) * EP + 4 * (lane >> 4);
   const float *er = ep + (lane >> 5) * EP + (lane & 31) * 4;
 #pragma unroll
-  for (int i = 0; i < I; ++i) {
+  for (int i = 0; i < TM / 32; ++i) {
     // accumulate: read this block's destination first, so the loads are in
     // flight during the LDS round trip instead of one dependent load per row
     float4 pre[16];
@@ -598,13 +612,15 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
         }
       }
     }
+    // block rows 2i and 2i+1: lane holds row (lane & 15) of each, four
+    // consecutive columns 16 j + 4 (lane >> 4) .. +3 of every column block j
 #pragma unroll
-    for (int j = 0; j < J; ++j)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4 *>(ew + j * 32 + 8 * q) =
-            make_float4(__builtin_ldexpf(acc[i][j][4 * q], e), __builtin_ldexpf(acc[i][j][4 * q + 1], e),
-                        __builtin_ldexpf(acc[i][j][4 * q + 2], e), __builtin_ldexpf(acc[i][j][4 * q + 3], e));
+      for (int j = 0; j < J; ++j)
+        *reinterpret_cast<float4 *>(ew + h * 16 * EP + j * 16) =
+            make_float4(__builtin_ldexpf(acc[2 * i + h][j][0], e), __builtin_ldexpf(acc[2 * i + h][j][1], e),
+                        __builtin_ldexpf(acc[2 * i + h][j][2], e), __builtin_ldexpf(acc[2 * i + h][j][3], e));
     // same wave writes then reads its own LDS rows: LDS operations of one wave
     // complete in order
     if (fast) {
@@ -713,11 +729,12 @@ hipError_t launch_fmts(const GemmParams &g, hipStream_t s) {
 }  // namespace
 
 // Relative cost of a round of tiles against a round of 256 x 256 ones at the
-// same K, measured on MI355X (K = 4096): 256 x 192 or 192 x 256 ~0.76 (0.75
-// of the MFMA work at a slightly lower efficiency per FLOP), the 8-wave
-// 256 x 128 kernel ~0.68.  Rounded up, so a tie keeps the larger tile.
-constexpr double kCost192 = 0.80;
-constexpr double kCost128 = 0.70;
+// same K, measured on MI355X (K = 4096, one round of each shape, bf16 out):
+// 256 x 192 0.89, 192 x 256 0.86 (0.75 of the MFMA work at a lower
+// efficiency per FLOP), the 8-wave 256 x 128 kernel 0.905.  Rounded up, so a
+// tie keeps the larger tile.
+constexpr double kCost192 = 0.90;
+constexpr double kCost128 = 0.92;
 
 static std::atomic<int> g_tile_override{0};
 

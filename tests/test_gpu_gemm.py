@@ -222,9 +222,11 @@ def test_forced_tile_shapes_exact(forced_tile, tile, shape):
 
 
 @pytest.mark.parametrize("shape", [(768, 768, 1000), (1000, 700, 320), (576, 4096, 384)], ids=str)
-def test_four_wave_tile_shapes_same_bits(forced_tile, shape):
-    """256x256, 256x192 and 192x256 run the same MFMA in the same K order: on
-    random codes (inexact FP32 sums) their outputs are bit-identical."""
+def test_tile_shapes_same_bits(forced_tile, shape):
+    """Every macro-tile shape (256x256, 256x192, 192x256 with four waves,
+    256x128 with eight) runs the same MFMA with the same reduction bytes per
+    lane in the same K order: on random codes (inexact FP32 sums) their outputs
+    are bit-identical."""
     qe = forced_tile
     d = dev()
     m, n, k = shape
@@ -232,10 +234,10 @@ def test_four_wave_tile_shapes_same_bits(forced_tile, shape):
     A = random_codes(rng, m, k, 0, rup16(k))
     B = random_codes(rng, n, k, 1, rup16(k))
     outs = []
-    for tile in (1, 2, 3):
+    for tile in (1, 2, 3, 4):
         assert qe.qe_set_gemm_tile(tile) == "OK"
         outs.append(run_gemm(qe, d, A, 0, B, 1, m, n, k, 2.0 ** -2, 2.0 ** 3, qe.F32, n)[: m * n])
     ref = gemm.gemm_tn(A[:, :k], "E4M3", B[:, :k], "E5M2", 2.0 ** -2, 2.0 ** 3)
     assert rel_err(outs[0].reshape(m, n), ref) <= 1e-3
-    np.testing.assert_array_equal(outs[1], outs[0])
-    np.testing.assert_array_equal(outs[2], outs[0])
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o, outs[0])
