@@ -771,7 +771,7 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   // Tile choice by wave quantization: each CU runs one workgroup at a time, so
   // a grid costs ceil(tiles / CUs) rounds of one tile's time; the smaller tiles
   // win where the 256 x 256 grid leaves its last round mostly empty (N = 6144:
-  // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.76).
+  // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.89).
   auto rounds = [&](int64_t bm, int64_t bn) {
     const int64_t t = ((g.m + bm - 1) / bm) * ((g.n + bn - 1) / bn);
     return double((t + kCUs - 1) / kCUs);

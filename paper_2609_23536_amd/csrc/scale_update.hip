@@ -38,17 +38,31 @@ __global__ __launch_bounds__(kThreads) void scale_update_kernel(UpdateParams p) 
   // amax values are >= +0 or a positive-signed NaN, so their bit patterns order
   // like the values, and every NaN pattern sorts above +inf.
   // The role's amax accumulator (if any) is folded into history[0] and cleared.
-  uint32_t acc = 0;
-  if (m.accum != nullptr && tid < kAmaxLines) {
-    acc = __float_as_uint(m.accum[tid * kAmaxStride]) & 0x7fffffffu;
-    m.accum[tid * kAmaxStride] = 0.0f;
+  // All global reads are issued before the first store (the accumulator's
+  // clear), so they overlap instead of paying two memory latencies in a row.
+  const bool has_acc = m.accum != nullptr && tid < kAmaxLines;
+  uint32_t acc = has_acc ? __float_as_uint(m.accum[tid * kAmaxStride]) & 0x7fffffffu : 0u;
+  constexpr int kPre = 4;  // history elements per lane read up front (H <= 1024)
+  uint32_t pre[kPre];
+#pragma unroll
+  for (int k = 0; k < kPre; ++k) {
+    const int i = tid + k * kThreads;
+    pre[k] = i < H ? __float_as_uint(m.hist[i]) & 0x7fffffffu : 0u;
   }
   acc = wave_max_u32(acc);  // wave 0 holds the accumulator's value, the other waves 0
+  if (has_acc) m.accum[tid * kAmaxStride] = 0.0f;
 
   uint32_t mx = 0;
-  for (int i = tid; i < H; i += kThreads) {
-    uint32_t b = __float_as_uint(m.hist[i]) & 0x7fffffffu;
+#pragma unroll
+  for (int k = 0; k < kPre; ++k) {
+    const int i = tid + k * kThreads;
+    uint32_t b = pre[k];
     if (i == 0) b = b > acc ? b : acc;  // i == 0 only on lane 0 of wave 0
+    if (i < H) hist_sh[i] = b;
+    mx = b > mx ? b : mx;
+  }
+  for (int i = tid + kPre * kThreads; i < H; i += kThreads) {
+    const uint32_t b = __float_as_uint(m.hist[i]) & 0x7fffffffu;
     hist_sh[i] = b;
     mx = b > mx ? b : mx;
   }
