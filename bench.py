@@ -7,7 +7,10 @@ Llama-3-8B shape by default, 4096 tokens, bf16 inputs and master weights,
 amax history 1024):  F (with the weight-cache refresh, since every step
 follows a version bump), then dI and the deferred dW with direct placement
 into one flat FP32 main-gradient buffer, then arena finalize and optimizer
-commit.  Every action is one HIP-graph replay behind the two-way handoff.
+commit.  Every action is one HIP-graph replay, by default on the caller's
+stream (stream order gives both directions of the handoff; --executor two-way
+runs the paper's two-way handoff through the library's graph stream instead,
+and the line reports the other executor's step time beside the headline).
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
 
 Prints one JSON line.  `value` is GEMM FLOPs (fwd + dI + dW, 2*M*N*K each)
@@ -45,6 +48,10 @@ def parse():
                     help="skip the copied-gradient passes (direct placement only)")
     ap.add_argument("--no-current", action="store_true", help="skip the current-scaling passes")
     ap.add_argument("--no-checkpoint", action="store_true", help="skip the checkpoint / restart measurement")
+    ap.add_argument("--executor", choices=("caller", "two-way"), default="caller",
+                    help="caller: every action replayed on the caller's stream (stream order is the handoff); "
+                         "two-way: on the library's graph stream behind the paper's two-way handoff")
+    ap.add_argument("--no-executor", action="store_true", help="skip the pass with the other executor")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-action latency of the small single-linear schedule")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
@@ -85,10 +92,12 @@ def copy_calibration(nbytes):
 
 
 class StageBench:
-    def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False, current=False):
+    def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False, current=False,
+                 replay_on_caller=False):
         import workloads as W
         self.qe, self.torch, self.wl, self.d = qe, torch, wl, device
-        self.ctx = qe.Context(1, use_graphs=use_graphs, copy_gradients=copy_gradients)
+        self.ctx = qe.Context(1, use_graphs=use_graphs, copy_gradients=copy_gradients,
+                              replay_on_caller=replay_on_caller)
         self.n_lin = len(wl.linears)
         bf = wl.in_dtype == "bf16"
         self.dt = qe.BF16 if bf else qe.F32
@@ -151,8 +160,8 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
         return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
 
     res = {}
-    for mode in ("graph", "eager"):
-        ctx = qe.Context(wl.microbatches, use_graphs=(mode == "graph"))
+    for mode in ("graph", "eager", "graph_on_caller"):
+        ctx = qe.Context(wl.microbatches, use_graphs=(mode != "eager"), replay_on_caller=(mode == "graph_on_caller"))
         w = up(W.layer_weight(wl, 0))
         st, idx = ctx.qe_layer_register(0, 0, lin.n_out, lin.k_in, wl.tokens, w, qe.F32, wl.history, wl.margin)
         assert st == "OK" and idx == 0, st
@@ -197,7 +206,8 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
         ctx.close()
     return {"workload": wl.key, "actions_per_step": 3 * wl.microbatches,
             "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
-            "eager_over_graph": round(res["eager"] / res["graph"], 3)}
+            "eager_over_graph": round(res["eager"] / res["graph"], 3),
+            "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2)}
 
 
 def timed_ms(b, torch, warmup, steps):
@@ -284,7 +294,8 @@ def main():
     wl = W.WORKLOADS[args.workload]
     use_graphs = not args.eager
 
-    b = StageBench(qe, torch, wl, use_graphs, dev)
+    on_caller = args.executor == "caller"
+    b = StageBench(qe, torch, wl, use_graphs, dev, replay_on_caller=on_caller)
     for _ in range(args.warmup):
         b.step()
     torch.cuda.synchronize()
@@ -313,7 +324,7 @@ def main():
     del b
     torch.cuda.empty_cache()
     if not args.no_checkpoint:
-        r = StageBench(qe, torch, wl, use_graphs, dev)
+        r = StageBench(qe, torch, wl, use_graphs, dev, replay_on_caller=on_caller)
         r.epoch = epoch
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -339,7 +350,7 @@ def main():
     # into the view) against direct placement, same steps, same replay mode
     copied_ms = None
     if not args.no_ablation:
-        c = StageBench(qe, torch, wl, use_graphs, dev, copy_gradients=True)
+        c = StageBench(qe, torch, wl, use_graphs, dev, copy_gradients=True, replay_on_caller=on_caller)
         copied_ms = timed_ms(c, torch, args.warmup, args.steps)
         c.ctx.close()
         del c
@@ -348,11 +359,24 @@ def main():
     # current (dynamic) scaling: the same step with every cast scaled by its own tensor's amax
     current_ms = None
     if not args.no_current:
-        c = StageBench(qe, torch, wl, use_graphs, dev, current=True)
+        c = StageBench(qe, torch, wl, use_graphs, dev, current=True, replay_on_caller=on_caller)
         current_ms = timed_ms(c, torch, args.warmup, args.steps)
         assert c.ctx.qe_sync() == "OK"
         cst = c.ctx.qe_get_state()
         assert cst["device_token"] == cst["token"]
+        c.ctx.close()
+        del c
+        torch.cuda.empty_cache()
+
+    # the other executor on the same steps: the paper's two-way handoff through
+    # the graph stream, or (with --executor two-way) replay on the caller's stream
+    other_ms = None
+    if not args.no_executor:
+        c = StageBench(qe, torch, wl, use_graphs, dev, replay_on_caller=not on_caller)
+        other_ms = timed_ms(c, torch, args.warmup, args.steps)
+        assert c.ctx.qe_sync() == "OK"
+        cst = c.ctx.qe_get_state()
+        assert cst["device_token"] == cst["token"] and (cst["handoffs"] == 0) == (not on_caller)
         c.ctx.close()
         del c
         torch.cuda.empty_cache()
@@ -400,7 +424,8 @@ def main():
         "vs_baseline": None, "dtype": "fp8(e4m3 x,w / e5m2 dy), f32 accumulate", "data": "synthetic",
         "config": {"workload": wl.key, "tokens": wl.tokens, "microbatches": wl.microbatches,
                    "linears": [[l.name, l.k_in, l.n_out] for l in wl.linears], "in_dtype": wl.in_dtype,
-                   "amax_history": wl.history, "graphs": use_graphs},
+                   "amax_history": wl.history, "graphs": use_graphs,
+                   "executor": "replay_on_caller" if on_caller else "graph_stream_two_way_handoff"},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4),
@@ -431,6 +456,11 @@ def main():
                      "launches": a_n, "bytes_per_step": amax_bytes(wl)},
             "quantize": {"achieved": round(cq_gbs, 1), "unit": "GB/s", "frac": round(cq_gbs / HBM_PEAK_GBS, 4),
                          "avg_launch_us": round(cq_ms / cq_n * 1e3, 2), "launches": cq_n}}
+    if other_ms is not None:
+        out["executor_" + ("two_way_handoff" if on_caller else "replay_on_caller")] = {
+            "ms_per_step": round(other_ms, 4), "value": round(flops / (other_ms * 1e-3) / 1e12, 2),
+            "unit": "TFLOP/s", "step_time_vs_headline": round(other_ms / ms, 4),
+            "handoffs_per_step": 2 * 3 * wl.microbatches * len(wl.linears) if on_caller else 0}
     if latency is not None:
         out["per_action_latency"] = latency
     if not args.no_cpu_baseline:

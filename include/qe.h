@@ -214,7 +214,17 @@ typedef struct {
   int32_t one_way_handoff; /* testing only: skip the caller's wait on the graph tail (§2.3) */
   int32_t copy_gradients;  /* 1: dW goes to a private FP32 buffer, then is copied into the bound view
                               (the copied-gradient path of §3.4, an ablation baseline); 0: direct */
-  int32_t reserved[2];
+  int32_t replay_on_caller; /* 0 (default): every action runs on the library's graph stream behind the
+                              two-way handoff of §2.3 / §4.4 (the graph stream waits on the caller's
+                              event, the caller waits on the graph's tail event).  1: every action's
+                              graph (or kernels) is launched on the caller's stream itself, so stream
+                              order gives both directions of the handoff with no cross-stream event;
+                              when an action comes from another stream than the previous action, that
+                              stream first waits on an event recorded on the previous action's stream,
+                              so all actions of the context stay in one total order, as on one graph
+                              stream.  The same ordering contract, without the two cross-stream waits
+                              per action (each costs microseconds of device time on MI355X). */
+  int32_t reserved;
 } qe_config;
 
 typedef struct {
@@ -230,7 +240,8 @@ typedef struct {
 } qe_layer_desc;
 
 /* Create a context.  Allocates the graph stream and events (unless
- * null_executor).  Errors: QE_ERR_INVALID_ARG, QE_ERR_UNSUPPORTED, QE_ERR_HIP. */
+ * null_executor).  Errors: QE_ERR_INVALID_ARG (also replay_on_caller outside
+ * {0, 1}, or together with one_way_handoff), QE_ERR_UNSUPPORTED, QE_ERR_HIP. */
 qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host);
 void qe_ctx_destroy(qe_ctx *ctx);
 

@@ -116,6 +116,11 @@ struct qe_ctx {
   qe::Contract contract;
   hipStream_t gs = nullptr;
   hipEvent_t ev_in = nullptr, ev_tail = nullptr;
+  // replay_on_caller: the stream of the previous action, and the event that
+  // chains the next action to it when the stream changes
+  bool has_last = false;
+  hipStream_t last = nullptr;
+  hipEvent_t ev_chain = nullptr;
   long long *d_token = nullptr;
   std::vector<LayerDev> layers;
   std::map<uint64_t, GraphEntry> graphs;
@@ -155,31 +160,48 @@ hipEvent_t pooled_event(qe_ctx *c) {
   return e;
 }
 
-hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed) {
+hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed, hipStream_t s) {
   for (const Call &call : plan) {
     if (timed) {
       TimedCall t{call.kind, pooled_event(c), pooled_event(c)};
       if (!t.t0 || !t.t1) return hipErrorOutOfMemory;
-      hipError_t e = hipEventRecord(t.t0, c->gs);
+      hipError_t e = hipEventRecord(t.t0, s);
       if (e != hipSuccess) return e;
-      e = launch(call, c->gs);
+      e = launch(call, s);
       if (e != hipSuccess) return e;
-      e = hipEventRecord(t.t1, c->gs);
+      e = hipEventRecord(t.t1, s);
       if (e != hipSuccess) return e;
       c->timed.push_back(t);
     } else {
-      const hipError_t e = launch(call, c->gs);
+      const hipError_t e = launch(call, s);
       if (e != hipSuccess) return e;
     }
   }
   return hipSuccess;
 }
 
+// Wait for every action enqueued so far: the graph stream, and with
+// replay_on_caller the stream of the last action (earlier actions precede it
+// in the chained order).
+hipError_t sync_actions(qe_ctx *c) {
+  hipError_t e = hipStreamSynchronize(c->gs);
+  if (e == hipSuccess && c->has_last && c->last != c->gs) e = hipStreamSynchronize(c->last);
+  return e;
+}
+
 // Two-way handoff around one action (§2.3, §4.4).
 qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller) {
   DeviceGuard dg(c->cfg.device);
   if (!dg.ok) return QE_ERR_HIP;
-  if (caller != c->gs) {
+  const bool on_caller = c->cfg.replay_on_caller != 0;
+  const hipStream_t s = on_caller ? caller : c->gs;
+  if (on_caller) {
+    // stream order covers both directions; only a change of stream needs an edge
+    if (c->has_last && c->last != caller) {
+      if (hipEventRecord(c->ev_chain, c->last) != hipSuccess) return QE_ERR_HIP;
+      if (hipStreamWaitEvent(caller, c->ev_chain, 0) != hipSuccess) return QE_ERR_HIP;
+    }
+  } else if (caller != c->gs) {
     if (hipEventRecord(c->ev_in, caller) != hipSuccess) return QE_ERR_HIP;
     if (hipStreamWaitEvent(c->gs, c->ev_in, 0) != hipSuccess) return QE_ERR_HIP;
   }
@@ -193,7 +215,7 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
       }
       hipGraph_t graph = nullptr;
       if (hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal) != hipSuccess) return QE_ERR_HIP;
-      const hipError_t le = enqueue(c, plan, false);
+      const hipError_t le = enqueue(c, plan, false, c->gs);
       const hipError_t ce = hipStreamEndCapture(c->gs, &graph);
       if (le != hipSuccess || ce != hipSuccess || graph == nullptr) {
         if (graph) (void)hipGraphDestroy(graph);
@@ -210,10 +232,15 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
       c->st.capture_ns +=
           std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
     }
-    if (hipGraphLaunch(e.exec, c->gs) != hipSuccess) return QE_ERR_HIP;
+    if (hipGraphLaunch(e.exec, s) != hipSuccess) return QE_ERR_HIP;
     c->st.replays += 1;
   } else {
-    if (enqueue(c, plan, c->timing != 0) != hipSuccess) return QE_ERR_HIP;
+    if (enqueue(c, plan, c->timing != 0, s) != hipSuccess) return QE_ERR_HIP;
+  }
+  if (on_caller) {
+    c->has_last = true;
+    c->last = s;
+    return QE_OK;
   }
   if (hipEventRecord(c->ev_tail, c->gs) != hipSuccess) return QE_ERR_HIP;
   if (!c->cfg.one_way_handoff && caller != c->gs) {
@@ -568,6 +595,9 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
 qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
   if (cfg_host == nullptr || out_host == nullptr || cfg_host->microbatches < 1 || cfg_host->microbatches > 4096)
     return QE_ERR_INVALID_ARG;
+  // the one-way (testing) handoff only exists for the graph stream
+  if (cfg_host->replay_on_caller != 0 && (cfg_host->replay_on_caller != 1 || cfg_host->one_way_handoff != 0))
+    return QE_ERR_INVALID_ARG;
   *out_host = nullptr;
   qe_ctx *c = new (std::nothrow) qe_ctx(*cfg_host);
   if (c == nullptr) return QE_ERR_HIP;
@@ -591,6 +621,7 @@ qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
     // it the caller may hand results to the host or to a copy engine.
     ok = ok && hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming | hipEventDisableSystemFence) == hipSuccess;
     ok = ok && hipEventCreateWithFlags(&c->ev_tail, hipEventDisableTiming) == hipSuccess;
+    ok = ok && hipEventCreateWithFlags(&c->ev_chain, hipEventDisableTiming) == hipSuccess;
     ok = ok && hipMalloc(reinterpret_cast<void **>(&c->d_token), sizeof(long long)) == hipSuccess;
     ok = ok && hipMemset(c->d_token, 0, sizeof(long long)) == hipSuccess;
     if (!ok) {
@@ -606,7 +637,7 @@ void qe_ctx_destroy(qe_ctx *c) {
   if (c == nullptr) return;
   if (!c->cfg.null_executor) {
     DeviceGuard dg(c->cfg.device);
-    if (c->gs) (void)hipStreamSynchronize(c->gs);
+    if (c->gs) (void)sync_actions(c);
     for (auto &kv : c->graphs)
       if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
     for (auto &L : c->layers)
@@ -619,6 +650,7 @@ void qe_ctx_destroy(qe_ctx *c) {
     if (c->d_token) (void)hipFree(c->d_token);
     if (c->ev_in) (void)hipEventDestroy(c->ev_in);
     if (c->ev_tail) (void)hipEventDestroy(c->ev_tail);
+    if (c->ev_chain) (void)hipEventDestroy(c->ev_chain);
     if (c->gs) (void)hipStreamDestroy(c->gs);
   }
   delete c;
@@ -833,7 +865,7 @@ qe_status qe_checkpoint_export(qe_ctx *c, void *buf_host, int64_t capacity, int6
   if (buf_host == nullptr) return QE_OK;
   if (capacity < size) return QE_ERR_INVALID_ARG;
   DeviceGuard dg(c->cfg.device);
-  if (!c->cfg.null_executor && (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess)) return QE_ERR_HIP;
+  if (!c->cfg.null_executor && (!dg.ok || sync_actions(c) != hipSuccess)) return QE_ERR_HIP;
   std::vector<uint8_t> out(size_t(size), 0);
   uint8_t *w = out.data();
   CkptHeader h;
@@ -896,7 +928,7 @@ qe_status qe_checkpoint_import(qe_ctx *c, const void *buf_host, int64_t size) {
   if (q != QE_OK) return q;
   if (!c->cfg.null_executor) {
     DeviceGuard dg(c->cfg.device);
-    if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    if (!dg.ok || sync_actions(c) != hipSuccess) return QE_ERR_HIP;
     r = b + sizeof(h);
     std::vector<float> meta;
     for (const auto &L : c->layers) {
@@ -929,7 +961,7 @@ qe_status qe_sync(qe_ctx *c) {
   if (c == nullptr) return QE_ERR_INVALID_ARG;
   if (c->cfg.null_executor) return QE_OK;
   DeviceGuard dg(c->cfg.device);
-  if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+  if (!dg.ok || sync_actions(c) != hipSuccess) return QE_ERR_HIP;
   long long tok = 0;
   if (hipMemcpy(&tok, c->d_token, sizeof(tok), hipMemcpyDeviceToHost) != hipSuccess) return QE_ERR_HIP;
   c->st.device_token = tok;
@@ -996,7 +1028,7 @@ qe_status qe_get_kernel_timing(qe_ctx *c, int32_t kernel_class, double *total_ms
     return QE_ERR_INVALID_ARG;
   if (!c->cfg.null_executor && !c->timed.empty()) {
     DeviceGuard dg(c->cfg.device);
-    if (!dg.ok || hipStreamSynchronize(c->gs) != hipSuccess) return QE_ERR_HIP;
+    if (!dg.ok || sync_actions(c) != hipSuccess) return QE_ERR_HIP;
     for (auto &t : c->timed) {
       float ms = 0.f;
       if (hipEventElapsedTime(&ms, t.t0, t.t1) != hipSuccess) return QE_ERR_HIP;

@@ -52,7 +52,7 @@ class FP8Meta(C.Structure):
 class Config(C.Structure):
     _fields_ = [("device", C.c_int32), ("microbatches", C.c_int32), ("use_graphs", C.c_int32),
                 ("null_executor", C.c_int32), ("one_way_handoff", C.c_int32), ("copy_gradients", C.c_int32),
-                ("reserved", C.c_int32 * 2)]
+                ("replay_on_caller", C.c_int32), ("reserved", C.c_int32)]
 
 
 class LayerDesc(C.Structure):
@@ -213,9 +213,9 @@ class Context:
     """Owns one qe_ctx.  Methods forward to the C calls of the same name."""
 
     def __init__(self, microbatches: int, use_graphs: bool = False, null_executor: bool = False, device: int = 0,
-                 one_way_handoff: bool = False, copy_gradients: bool = False):
+                 one_way_handoff: bool = False, copy_gradients: bool = False, replay_on_caller: bool = False):
         cfg = Config(device, microbatches, int(use_graphs), int(null_executor), int(one_way_handoff),
-                     int(copy_gradients))
+                     int(copy_gradients), int(replay_on_caller))
         h = C.c_void_p()
         st = _st(lib().qe_ctx_create(C.byref(cfg), C.byref(h)))
         if st != "OK":

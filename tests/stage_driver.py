@@ -44,11 +44,17 @@ class Spec:
 
 
 class GpuStage:
-    def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False, weights=None):
-        """`weights`: the current master weights (workloads.Tensor per layer), default the initial ones."""
+    def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False, weights=None,
+                 replay_on_caller=False, streams=None):
+        """`weights`: the current master weights (workloads.Tensor per layer), default the initial ones.
+        `streams`: caller streams used in turn, one per action (inputs are uploaded and outputs
+        allocated on the action's stream); default torch's current stream."""
         self.qe, self.spec = qe, spec
         self.d = device
-        self.ctx = qe.Context(spec.M, use_graphs=use_graphs, copy_gradients=copy_gradients)
+        self.ctx = qe.Context(spec.M, use_graphs=use_graphs, copy_gradients=copy_gradients,
+                              replay_on_caller=replay_on_caller)
+        self.streams = streams
+        self.n_actions = 0
         dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
         self.w = [upload(spec.weight(u) if weights is None else weights[u], self.d) for u in range(len(spec.shapes))]
         for u, (n, k) in enumerate(spec.shapes):
@@ -74,35 +80,46 @@ class GpuStage:
         return self.qe.ACCUM if (u, off) in self.written else self.qe.INIT
 
     def run(self, schedule, epoch, step):
+        for a, m in schedule:
+            for u in range(len(self.spec.shapes)):
+                if self.streams:
+                    s = self.streams[self.n_actions % len(self.streams)]
+                    with torch.cuda.stream(s):
+                        self._action(a, m, u, epoch, step, s)
+                else:
+                    self._action(a, m, u, epoch, step, None)
+                self.n_actions += 1
+
+    def _action(self, a, m, u, epoch, step, caller):
         qe, spec = self.qe, self.spec
         dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
         odt = qe.BF16 if spec.out_dtype == "bf16" else qe.F32
-        for a, m in schedule:
-            for u, (n, k) in enumerate(spec.shapes):
-                key = qe.key(epoch, 0, m, u)
-                x, dy = spec.inputs(u, m, step)
-                if a == "F":
-                    y = self._out(spec.tokens, n)
-                    st, self.refs[(u, m)] = self.ctx.qe_fp8_linear_fwd(u, key, upload(x, self.d), dt, spec.tokens,
-                                                                       y, odt)
-                    self.outs[("y", u, m, step)] = y
-                elif a == "dI":
-                    dx = self._out(spec.tokens, k)
-                    st = self.ctx.qe_fp8_linear_dgrad(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt)
-                    self.outs[("dx", u, m, step)] = dx
-                elif a == "dW":
-                    mode = self._mode(u, m)
-                    st = self.ctx.qe_fp8_linear_wgrad_place(u, key, self.refs[(u, m)], self.grad, spec.offset(u, m),
-                                                            k, mode)
-                    self.written.add((u, spec.offset(u, m)))
-                else:
-                    dx = self._out(spec.tokens, k)
-                    mode = self._mode(u, m)
-                    st = self.ctx.qe_fp8_linear_bwd_full(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt,
-                                                         self.grad, spec.offset(u, m), k, mode)
-                    self.written.add((u, spec.offset(u, m)))
-                    self.outs[("dx", u, m, step)] = dx
-                assert st == "OK", (a, m, u, st)
+        n, k = spec.shapes[u]
+        key = qe.key(epoch, 0, m, u)
+        x, dy = spec.inputs(u, m, step)
+        if a == "F":
+            y = self._out(spec.tokens, n)
+            st, self.refs[(u, m)] = self.ctx.qe_fp8_linear_fwd(u, key, upload(x, self.d), dt, spec.tokens,
+                                                               y, odt, caller=caller)
+            self.outs[("y", u, m, step)] = y
+        elif a == "dI":
+            dx = self._out(spec.tokens, k)
+            st = self.ctx.qe_fp8_linear_dgrad(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt,
+                                             caller=caller)
+            self.outs[("dx", u, m, step)] = dx
+        elif a == "dW":
+            mode = self._mode(u, m)
+            st = self.ctx.qe_fp8_linear_wgrad_place(u, key, self.refs[(u, m)], self.grad, spec.offset(u, m),
+                                                    k, mode, caller=caller)
+            self.written.add((u, spec.offset(u, m)))
+        else:
+            dx = self._out(spec.tokens, k)
+            mode = self._mode(u, m)
+            st = self.ctx.qe_fp8_linear_bwd_full(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt,
+                                                 self.grad, spec.offset(u, m), k, mode, caller=caller)
+            self.written.add((u, spec.offset(u, m)))
+            self.outs[("dx", u, m, step)] = dx
+        assert st == "OK", (a, m, u, st)
 
     def end_step(self, new_weights=None):
         assert self.ctx.qe_arena_finalize() == "OK"
@@ -110,6 +127,7 @@ class GpuStage:
             torch.cuda.synchronize()
             for u, w in enumerate(new_weights):
                 self.w[u].copy_(upload(w, self.d))
+            torch.cuda.synchronize()  # the next actions may run on other streams
         assert self.ctx.qe_optimizer_commit() == "OK"
         self.written = set()
 

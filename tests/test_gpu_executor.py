@@ -1,0 +1,106 @@
+"""The caller-stream executor (qe_config.replay_on_caller): each action's graph
+or kernels run on the caller's stream, so stream order replaces the two-way
+handoff of §2.3 / §4.4, and a change of caller stream between actions is
+chained through one event so all actions keep one total order (the ordering
+the paper gets from a single graph stream).  Results must be bitwise those of
+the graph-stream executor, also with every action on a different stream, and a
+consumer enqueued on the caller stream right after an action must never see
+stale output."""
+import numpy as np
+import pytest
+
+from tests import schedules as S
+from tests.gpu_util import dev, torch
+from tests.libqe import need_lib
+from tests.stage_driver import GpuStage, OracleStage, Spec
+
+pytestmark = pytest.mark.gpu
+
+SPEC = Spec([(96, 160), (160, 64)], tokens=48, M=8, history=16, margin=0, in_dtype="bf16", shared_view=False, cfg=2)
+STEPS = [S.ZB_STEP0, S.ZB_STEP1, S.ZB_STEP0]
+
+
+def _run(use_graphs, replay_on_caller, n_streams=0):
+    qe = need_lib()
+    d = dev()
+    streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams else None
+    g = GpuStage(qe, SPEC, use_graphs=use_graphs, device=d, replay_on_caller=replay_on_caller, streams=streams)
+    o = OracleStage(SPEC)
+    grads = []
+    for step, sched in enumerate(STEPS):
+        g.run(sched, step, step)
+        o.run(sched, step, step)
+        torch.cuda.synchronize()
+        grads.append(g.grad.cpu().numpy().copy())
+        new_w = o.sgd_weights()
+        g.end_step(new_w)
+        o.end_step(new_w)
+    torch.cuda.synchronize()
+    outs = {k: v.cpu().numpy().copy() for k, v in g.outs.items()}
+    states = [g.fp8_state(u) for u in range(len(SPEC.shapes))]
+    assert g.ctx.qe_sync() == "OK"
+    st = g.ctx.qe_get_state()
+    assert st["device_token"] == st["token"]
+    return g, grads, outs, states, st
+
+
+def _same(a, b):
+    for x, y in zip(a[1], b[1]):
+        np.testing.assert_array_equal(x.view(np.uint32), y.view(np.uint32))
+    assert a[2].keys() == b[2].keys()
+    for k in a[2]:
+        np.testing.assert_array_equal(a[2][k], b[2][k], err_msg=str(k))
+    for x, y in zip(a[3], b[3]):
+        for r in x:
+            np.testing.assert_array_equal(x[r][0], y[r][0])
+            assert x[r][1:] == y[r][1:]
+
+
+@pytest.mark.parametrize("use_graphs", [False, True], ids=["eager", "graphs"])
+def test_caller_stream_bitwise_equals_graph_stream(use_graphs):
+    ref = _run(use_graphs, False)
+    got = _run(use_graphs, True)
+    _same(ref, got)
+    assert got[4]["handoffs"] == 0 and ref[4]["handoffs"] > 0
+    if use_graphs:
+        assert got[4]["replays"] == ref[4]["replays"] > 0
+
+
+@pytest.mark.parametrize("use_graphs", [False, True], ids=["eager", "graphs"])
+def test_caller_stream_chains_actions_across_streams(use_graphs):
+    """Every action on the next of three streams (F, dI and the deferred dW of
+    one microbatch on different streams; scale updates in fixed order across
+    them): the chaining event keeps one total order, bitwise as on one stream."""
+    ref = _run(use_graphs, False)
+    got = _run(use_graphs, True, n_streams=3)
+    _same(ref, got)
+
+
+def test_caller_stream_consumer_never_stale():
+    qe = need_lib()
+    d = dev()
+    n, k, t = 28672, 4096, 4096
+    ctx = qe.Context(1, use_graphs=True, replay_on_caller=True)
+    g = torch.Generator(device=d)
+    g.manual_seed(1)
+    w = (torch.randn(n, k, device=d, generator=g) * 0.02).to(torch.bfloat16)
+    x = torch.randn(t, k, device=d, generator=g).to(torch.bfloat16)
+    st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.BF16, 4, 0)
+    assert st == "OK"
+    y = torch.empty((t, n), dtype=torch.bfloat16, device=d)
+    caller = torch.cuda.Stream()
+    stale = 0
+    for trial in range(30):
+        with torch.cuda.stream(caller):
+            y.fill_(float("nan"))
+            st, ref = ctx.qe_fp8_linear_fwd(L, qe.key(0, 0, 0, 0), x, qe.BF16, t, y, qe.BF16, caller=caller)
+            assert st == "OK"
+            seen = y.clone()
+        torch.cuda.synchronize()
+        assert ctx.qe_sync() == "OK"
+        if not torch.equal(seen.view(torch.int16), y.view(torch.int16)):
+            stale += 1
+        assert ctx.qe_abort_epoch() == "OK" and ctx.qe_arena_rebuild() == "OK"
+    assert not torch.isnan(y.float()).any()
+    assert stale == 0
+    ctx.close()

@@ -262,6 +262,21 @@ def test_register_scaling_recipe_validation():
     c.close()
 
 
+def test_executor_config_validation():
+    """replay_on_caller is 0 or 1, and the one-way (testing) handoff exists only
+    for the graph-stream executor."""
+    qe = need_lib()
+    import ctypes as C
+    for replay, one_way, want in ((0, 0, "OK"), (1, 0, "OK"), (2, 0, "INVALID_ARG"), (-1, 0, "INVALID_ARG"),
+                                  (1, 1, "INVALID_ARG"), (0, 1, "OK")):
+        cfg = qe.Config(0, 1, 0, 1, one_way, 0, replay)
+        h = C.c_void_p()
+        st = qe.qe_status_str(qe.lib().qe_ctx_create(C.byref(cfg), C.byref(h)))
+        assert st == want, (replay, one_way, st)
+        if h:
+            qe.lib().qe_ctx_destroy(h)
+
+
 def _payload_fields(b):
     import struct
     magic, version, n_layers, M, _, e_w = struct.unpack_from("<8sIIiiq", b, 0)
