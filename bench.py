@@ -64,9 +64,10 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama3_8b_stage_4096tok_traf
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_23536_amd", "csrc", "gemm_fp8.hip")
 
 
-def gemm_traffic_per_launch():
+def gemm_traffic_per_launch(workload):
     """HBM bytes per GEMM launch from the committed counter runs, or None when
-    they were taken on a different GEMM kernel source than the current one."""
+    they were taken on another workload or a different GEMM kernel source than
+    the current one."""
     import hashlib
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -76,7 +77,7 @@ def gemm_traffic_per_launch():
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
     sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-    if kv.get("kernel_source_sha256") != sha:
+    if kv.get("kernel_source_sha256") != sha or kv.get("workload") != workload:
         return None
     return float(kv["gemm_hbm_bytes_per_launch"])
 
@@ -429,7 +430,7 @@ def main():
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4),
-                     "traffic": gemm_traffic_per_launch(),
+                     "traffic": gemm_traffic_per_launch(wl.key),
                      "kernel": "gemm_tn_w4_kernel / gemm_tn_kernel (fwd + dI + dW launches)",
                      "avg_launch_us": round(gemm_ms / gemm_n * 1e3, 2), "launches": gemm_n},
         "quantize": {"achieved": round(q_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
