@@ -52,6 +52,8 @@ def parse():
                     help="caller: every action replayed on the caller's stream (stream order is the handoff); "
                          "two-way: on the library's graph stream behind the paper's two-way handoff")
     ap.add_argument("--no-executor", action="store_true", help="skip the pass with the other executor")
+    ap.add_argument("--no-wgrad", action="store_true",
+                    help="skip the dW-placement measurement at the zero-bubble workload's 2048-token microbatch")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-action latency of the small single-linear schedule")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
@@ -209,6 +211,60 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
             "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
             "eager_over_graph": round(res["eager"] / res["graph"], 3),
             "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2)}
+
+
+def wgrad_place(qe, torch, device, tokens=2048, reps=20):
+    """The deferred dW GEMM with direct placement at the zero-bubble workload's
+    microbatch (2048 tokens) and the Llama-3-8B stage's four linears: dW =
+    dY^T X from the transposed E5M2 / E4M3 codes, INIT-placed into [N, K] views
+    of one flat FP32 buffer (each view at its own offset, as per microbatch).
+    Algorithmic bytes per launch: (N + K) * tokens code bytes read + 4 N K
+    written; roofline time max(FLOPs / MFMA peak, bytes / HBM peak)."""
+    import workloads as W
+    wl = W.WORKLOADS["llama3_8b_zb_8x2048"]
+    assert wl.tokens == tokens
+    one = torch.ones(1, device=device)
+    offs = wl.grad_offsets()
+    grad = torch.empty(wl.flat_grad_elems(), dtype=torch.float32, device=device)
+    tot_t = tot_b = tot_f = tot_roof = 0.0
+    per = []
+    for u, lin in enumerate(wl.linears):
+        n, k = lin.n_out, lin.k_in
+        g = torch.Generator(device=device)
+        g.manual_seed(u)
+        a = (torch.randn(n, tokens, device=device, generator=g) * 0.5).to(torch.float8_e5m2).view(torch.uint8)
+        b = (torch.randn(k, tokens, device=device, generator=g) * 0.5).to(torch.float8_e4m3fn).view(torch.uint8)
+        view = grad[offs[u]:]
+
+        def run():
+            st = qe.qe_fp8_gemm_tn(a, qe.E5M2, tokens, b, qe.E4M3, tokens, n, k, tokens, one, one, view, qe.F32, k,
+                                   qe.INIT)
+            assert st == "OK", st
+
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        e1.synchronize()
+        t = e0.elapsed_time(e1) / reps * 1e-3
+        byts = (n + k) * tokens + 4 * n * k
+        flop = 2.0 * n * k * tokens
+        roof = max(flop / (FP8_PEAK_TFLOPS * 1e12), byts / (HBM_PEAK_GBS * 1e9))
+        per.append({"linear": lin.name, "n": n, "k": k, "us": round(t * 1e6, 2), "gbs": round(byts / t / 1e9, 1),
+                    "tflops": round(flop / t / 1e12, 1), "roofline_frac": round(roof / t, 4),
+                    "bound": "hbm" if byts / (HBM_PEAK_GBS * 1e9) > flop / (FP8_PEAK_TFLOPS * 1e12) else "mfma"})
+        tot_t += t
+        tot_b += byts
+        tot_f += flop
+        tot_roof += roof
+    return {"workload": wl.key, "tokens": tokens, "placement": "INIT into per-view offsets of one flat FP32 buffer",
+            "achieved_gbs": round(tot_b / tot_t / 1e9, 1), "unit": "GB/s", "peak_gbs": HBM_PEAK_GBS,
+            "frac_hbm": round(tot_b / tot_t / 1e9 / HBM_PEAK_GBS, 4), "tflops": round(tot_f / tot_t / 1e12, 1),
+            "roofline_frac": round(tot_roof / tot_t, 4), "per_linear": per}
 
 
 def timed_ms(b, torch, warmup, steps):
@@ -383,6 +439,8 @@ def main():
         torch.cuda.empty_cache()
 
     latency = None if args.no_latency else per_action_latency(qe, torch, dev)
+    wgrad = None if args.no_wgrad else wgrad_place(qe, torch, dev)
+    torch.cuda.empty_cache()
 
     # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
     def instrumented(copy_gradients=False, current=False):
@@ -464,6 +522,8 @@ def main():
             "handoffs_per_step": 2 * 3 * wl.microbatches * len(wl.linears) if on_caller else 0}
     if latency is not None:
         out["per_action_latency"] = latency
+    if wgrad is not None:
+        out["wgrad_place"] = wgrad
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
     print(json.dumps(out), flush=True)
