@@ -1,6 +1,7 @@
 """Full-size parity on the Llama-3-8B-shaped stage in the benchmark's launch
-configuration (graph replay, 4096 tokens, bf16): two steps of F, dI and
-deferred dW for each linear, then
+configuration (graph replay on the caller's stream, 4096 tokens, bf16), and
+with the paper's graph-stream executor behind the two-way handoff: two steps
+of F, dI and deferred dW for each linear, then
 
 * amax histories and scales bit-exact (the oracle takes the amax of the full
   tensors, which is cheap);
@@ -25,11 +26,11 @@ def widen(t):
     return t.as_f32()
 
 
-@pytest.fixture(scope="module")
-def run():
+@pytest.fixture(scope="module", params=["replay_on_caller", "graph_stream"])
+def run(request):
     qe = need_lib()
     d = dev()
-    ctx = qe.Context(1, use_graphs=True)
+    ctx = qe.Context(1, use_graphs=True, replay_on_caller=request.param == "replay_on_caller")
     data, outs = [], []
     grad = torch.zeros(WL.flat_grad_elems(), dtype=torch.float32, device=d)
     offs = WL.grad_offsets()
