@@ -153,7 +153,8 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
     """Latency-bound case: one FP8 linear (K = N = 256), two microbatches of 128
     tokens, fp32 inputs, history 4, schedule F0 F1 dI0 dI1 dW0 dW1 (both dW into
     one shared view: INIT, then ACCUM), then finalize and commit.  Mean wall time
-    per action, graph replay behind the two-way handoff vs direct launches."""
+    per action: graph replay and direct launches, each behind the two-way
+    handoff (the graph stream) and on the caller's stream."""
     import numpy as np
     import workloads as W
     wl = W.WORKLOADS["single_linear_128x256x256"]
@@ -163,8 +164,8 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
         return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
 
     res = {}
-    for mode in ("graph", "eager", "graph_on_caller"):
-        ctx = qe.Context(wl.microbatches, use_graphs=(mode != "eager"), replay_on_caller=(mode == "graph_on_caller"))
+    for mode in ("graph", "eager", "graph_on_caller", "eager_on_caller"):
+        ctx = qe.Context(wl.microbatches, use_graphs=mode.startswith("graph"), replay_on_caller=mode.endswith("caller"))
         w = up(W.layer_weight(wl, 0))
         st, idx = ctx.qe_layer_register(0, 0, lin.n_out, lin.k_in, wl.tokens, w, qe.F32, wl.history, wl.margin)
         assert st == "OK" and idx == 0, st
@@ -210,7 +211,8 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
     return {"workload": wl.key, "actions_per_step": 3 * wl.microbatches,
             "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
             "eager_over_graph": round(res["eager"] / res["graph"], 3),
-            "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2)}
+            "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2),
+            "eager_on_caller_us_per_action": round(res["eager_on_caller"], 2)}
 
 
 def wgrad_place(qe, torch, device, tokens=2048, reps=20):
