@@ -218,12 +218,13 @@ typedef struct {
                               two-way handoff of §2.3 / §4.4 (the graph stream waits on the caller's
                               event, the caller waits on the graph's tail event).  1: every action's
                               graph (or kernels) is launched on the caller's stream itself, so stream
-                              order gives both directions of the handoff with no cross-stream event;
-                              when an action comes from another stream than the previous action, that
-                              stream first waits on an event recorded on the previous action's stream,
-                              so all actions of the context stay in one total order, as on one graph
-                              stream.  The same ordering contract, without the two cross-stream waits
-                              per action (each costs microseconds of device time on MI355X). */
+                              order gives both directions of the handoff; every action's stream
+                              first waits on an event recorded right after the previous action (on
+                              its stream), so actions issued from different streams stay in one
+                              total order, as on one graph stream (on the same stream the wait is
+                              already satisfied).  No caller stream handle is kept between actions.
+                              The same ordering contract, without the two cross-stream waits per
+                              action of the graph-stream executor. */
   int32_t reserved;
 } qe_config;
 

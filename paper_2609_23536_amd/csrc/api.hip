@@ -116,10 +116,10 @@ struct qe_ctx {
   qe::Contract contract;
   hipStream_t gs = nullptr;
   hipEvent_t ev_in = nullptr, ev_tail = nullptr;
-  // replay_on_caller: the stream of the previous action, and the event that
-  // chains the next action to it when the stream changes
+  // replay_on_caller: an event recorded on each action's stream right after
+  // the action; the next action's stream waits on it (no stream handle of
+  // the caller is kept, so a caller may destroy its streams between actions)
   bool has_last = false;
-  hipStream_t last = nullptr;
   hipEvent_t ev_chain = nullptr;
   long long *d_token = nullptr;
   std::vector<LayerDev> layers;
@@ -181,11 +181,11 @@ hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed, hipStream_t s) {
 }
 
 // Wait for every action enqueued so far: the graph stream, and with
-// replay_on_caller the stream of the last action (earlier actions precede it
-// in the chained order).
+// replay_on_caller the chaining event of the last action (earlier actions
+// precede it in the chained order).
 hipError_t sync_actions(qe_ctx *c) {
   hipError_t e = hipStreamSynchronize(c->gs);
-  if (e == hipSuccess && c->has_last && c->last != c->gs) e = hipStreamSynchronize(c->last);
+  if (e == hipSuccess && c->has_last) e = hipEventSynchronize(c->ev_chain);
   return e;
 }
 
@@ -196,11 +196,10 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
   const bool on_caller = c->cfg.replay_on_caller != 0;
   const hipStream_t s = on_caller ? caller : c->gs;
   if (on_caller) {
-    // stream order covers both directions; only a change of stream needs an edge
-    if (c->has_last && c->last != caller) {
-      if (hipEventRecord(c->ev_chain, c->last) != hipSuccess) return QE_ERR_HIP;
-      if (hipStreamWaitEvent(caller, c->ev_chain, 0) != hipSuccess) return QE_ERR_HIP;
-    }
+    // Stream order covers both directions of the handoff.  The wait on the
+    // previous action's event orders actions issued from different streams;
+    // on the same stream it is already satisfied by stream order.
+    if (c->has_last && hipStreamWaitEvent(caller, c->ev_chain, 0) != hipSuccess) return QE_ERR_HIP;
   } else if (caller != c->gs) {
     if (hipEventRecord(c->ev_in, caller) != hipSuccess) return QE_ERR_HIP;
     if (hipStreamWaitEvent(c->gs, c->ev_in, 0) != hipSuccess) return QE_ERR_HIP;
@@ -238,8 +237,8 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
     if (enqueue(c, plan, c->timing != 0, s) != hipSuccess) return QE_ERR_HIP;
   }
   if (on_caller) {
+    if (hipEventRecord(c->ev_chain, s) != hipSuccess) return QE_ERR_HIP;
     c->has_last = true;
-    c->last = s;
     return QE_OK;
   }
   if (hipEventRecord(c->ev_tail, c->gs) != hipSuccess) return QE_ERR_HIP;
