@@ -104,3 +104,57 @@ def test_caller_stream_consumer_never_stale():
     assert not torch.isnan(y.float()).any()
     assert stale == 0
     ctx.close()
+
+
+def test_caller_stream_destroyed_between_actions():
+    """The caller-stream executor keeps no caller stream handle between actions:
+    F on a raw HIP stream that is destroyed right after the call (without a
+    synchronisation), then dI and dW on a second raw stream, give the same bits
+    as the same actions on torch's current stream."""
+    import ctypes as C
+    qe = need_lib()
+    d = dev()
+    hip = C.CDLL("libamdhip64.so")
+    n, k, t = 256, 256, 128
+    g = torch.Generator(device=d)
+    g.manual_seed(7)
+    w = torch.randn(n, k, device=d, generator=g) * 0.02
+    x = torch.randn(t, k, device=d, generator=g)
+    dy = torch.randn(t, n, device=d, generator=g) * 0.01
+
+    def run(raw):
+        ctx = qe.Context(1, use_graphs=True, replay_on_caller=True)
+        st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.F32, 4, 0)
+        assert st == "OK"
+        grad = torch.zeros(n * k, device=d)
+        assert ctx.qe_arena_bind(L, 0, grad, n * k, 0, k) == "OK"
+        y = torch.zeros(t, n, device=d)
+        dx = torch.zeros(t, k, device=d)
+        torch.cuda.synchronize()
+        for step in range(2):
+            key = qe.key(step, 0, 0, 0)
+            s1, s2 = C.c_void_p(), C.c_void_p()
+            if raw:
+                assert hip.hipStreamCreate(C.byref(s1)) == 0 and hip.hipStreamCreate(C.byref(s2)) == 0
+            st, ref = ctx.qe_fp8_linear_fwd(L, key, x, qe.F32, t, y, qe.F32, caller=s1.value if raw else None)
+            assert st == "OK"
+            if raw:
+                assert hip.hipStreamDestroy(s1) == 0       # no synchronisation first
+            c2 = s2.value if raw else None
+            assert ctx.qe_fp8_linear_dgrad(L, key, ref, dy, qe.F32, dx, qe.F32, caller=c2) == "OK"
+            assert ctx.qe_fp8_linear_wgrad_place(L, key, ref, grad, 0, k, qe.INIT, caller=c2) == "OK"
+            assert ctx.qe_sync() == "OK"
+            if raw:
+                assert hip.hipStreamDestroy(s2) == 0
+            assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+        torch.cuda.synchronize()
+        out = (y.cpu().numpy().copy(), dx.cpu().numpy().copy(), grad.cpu().numpy().copy())
+        st = ctx.qe_get_state()
+        assert st["device_token"] == st["token"]
+        ctx.close()
+        return out
+
+    ref = run(False)
+    got = run(True)
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
