@@ -375,7 +375,10 @@ qe_status qe_checkpoint_export(qe_ctx *ctx, void *buf_host, int64_t capacity, in
  * the FP8 state is undefined; discard the context. */
 qe_status qe_checkpoint_import(qe_ctx *ctx, const void *buf_host, int64_t size);
 
-/* Block until all device work of the context has finished. */
+/* Block until all device work of the context's actions has finished (the
+ * graph stream, and with replay_on_caller the last action's chaining event,
+ * which every earlier action precedes), then read back the device effect
+ * token. */
 qe_status qe_sync(qe_ctx *ctx);
 
 typedef struct {
@@ -386,7 +389,7 @@ typedef struct {
   int64_t graphs;            /* graph executables held */
   int64_t captures;          /* captures performed (incl. re-captures after a pointer change) */
   int64_t replays;           /* graph launches */
-  int64_t handoffs;          /* caller<->graph stream handoffs (2 per action) */
+  int64_t handoffs;          /* caller<->graph stream handoffs (2 per action; 0 with replay_on_caller) */
   int64_t capture_ns;        /* host time spent capturing + instantiating */
   int64_t arena_bytes;       /* bytes covered by bound views */
   int64_t device_bytes;      /* bytes the library allocated */
@@ -421,7 +424,7 @@ qe_status qe_get_slot_state(const qe_ctx *ctx, int32_t layer, int32_t slot, qe_s
 qe_status qe_inject_fault(qe_ctx *ctx, int32_t n);
 
 /* Kernel timing: when enabled (eager mode only), every kernel the context
- * launches is bracketed by HIP events on the graph stream; totals per kernel
+ * launches is bracketed by HIP events on the stream it runs on; totals per kernel
  * class (0 quantize, 1 scale update, 2 GEMM, 3 gradient copy) are read after
  * a qe_sync. */
 qe_status qe_set_kernel_timing(qe_ctx *ctx, int32_t enable);

@@ -189,7 +189,10 @@ hipError_t sync_actions(qe_ctx *c) {
   return e;
 }
 
-// Two-way handoff around one action (§2.3, §4.4).
+// One action's kernel sequence, captured once per (layer, action, slot) and
+// replayed, or launched directly.  Graph-stream executor: the two-way handoff
+// around it (§2.3, §4.4).  replay_on_caller: launched on the caller's stream,
+// chained to the previous action through ev_chain.
 qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller) {
   DeviceGuard dg(c->cfg.device);
   if (!dg.ok) return QE_ERR_HIP;
