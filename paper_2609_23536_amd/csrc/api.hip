@@ -58,6 +58,10 @@ struct Call {
     qe::GradCopyParams c;
     qe::AmaxParams a;
   };
+  // KC_QUANT only: a second, independent cast of the same input dtype and
+  // FP8 format that runs in the same launch (has_q2 != 0)
+  qe::QuantParams q2;
+  int32_t has_q2, pad2;
   Call() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
 };
 using Plan = std::vector<Call>;
@@ -141,7 +145,7 @@ bool elem_aligned(const void *p, int dt) { return uintptr_t(p) % (dt == QE_BF16 
 
 hipError_t launch(const Call &c, hipStream_t s) {
   switch (c.kind) {
-    case qe::KC_QUANT: return qe::launch_quantize(c.q, s);
+    case qe::KC_QUANT: return c.has_q2 ? qe::launch_quantize_pair(c.q, c.q2, s) : qe::launch_quantize(c.q, s);
     case qe::KC_UPDATE: return qe::launch_scale_update(c.u, s);
     case qe::KC_COPY: return qe::launch_grad_copy(c.c, s);
     case qe::KC_AMAX: return qe::launch_amax(c.a, s);
@@ -278,6 +282,20 @@ Call quant_call(const void *in, int in_dt, int64_t rows, int64_t cols, const qe:
   return c;
 }
 
+// Appends two independent casts; with the same input dtype and FP8 format
+// they share one launch.
+void push_quant_pair(Plan &p, const Call &a, const Call &b) {
+  if (a.q.in_bf16 == b.q.in_bf16 && a.q.fmt == b.q.fmt) {
+    Call c = a;
+    c.q2 = b.q;
+    c.has_q2 = 1;
+    p.push_back(c);
+  } else {
+    p.push_back(a);
+    p.push_back(b);
+  }
+}
+
 Call gemm_call(const uint8_t *a, int fa, int64_t lda, const uint8_t *b, int fb, int64_t ldb, int64_t m, int64_t n,
                int64_t k, const float *sa, const float *sb, void *cptr, int c_dt, int64_t ldc, int mode) {
   Call c;
@@ -326,19 +344,24 @@ Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt,
     if (refresh) p.push_back(amax_call(d.w, d.w_dtype, d.n_out * d.k_in, L.role(QE_ROLE_W)));
     p.push_back(amax_call(x, x_dt, tokens * d.k_in, L.role(QE_ROLE_X)));
     p.push_back(refresh ? update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token) : update_call(L, {QE_ROLE_X}, c->d_token));
+    const Call qx =
+        quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv, false);
     if (refresh)
-      p.push_back(quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt,
-                             L.w_sinv, false));
-    p.push_back(
-        quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv, false));
+      push_quant_pair(p, quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t,
+                                    L.ld_wqt, L.w_sinv, false), qx);
+    else
+      p.push_back(qx);
     p.push_back(gemm_call(L.x_q, d.fmt_x, L.ld_xq, L.w_q, d.fmt_w, L.ld_wq, tokens, d.n_out, d.k_in, S.x_sinv,
                           L.w_sinv, y, y_dt, d.n_out, QE_PLACE_INIT));
     return p;
   }
+  const Call qx = quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv);
   if (refresh)
-    p.push_back(quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt,
-                           L.w_sinv));
-  p.push_back(quant_call(x, x_dt, tokens, d.k_in, L.role(QE_ROLE_X), L.x_q, L.ld_xq, S.x_q_t, L.ld_t, S.x_sinv));
+    push_quant_pair(
+        p, quant_call(d.w, d.w_dtype, d.n_out, d.k_in, L.role(QE_ROLE_W), L.w_q, L.ld_wq, L.w_q_t, L.ld_wqt, L.w_sinv),
+        qx);
+  else
+    p.push_back(qx);
   p.push_back(gemm_call(L.x_q, d.fmt_x, L.ld_xq, L.w_q, d.fmt_w, L.ld_wq, tokens, d.n_out, d.k_in, S.x_sinv, L.w_sinv,
                         y, y_dt, d.n_out, QE_PLACE_INIT));
   p.push_back(update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token));

@@ -100,6 +100,8 @@ enum KernelClass { KC_QUANT = 0, KC_UPDATE = 1, KC_GEMM = 2, KC_COPY = 3, KC_AMA
 
 hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s);
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
+// Two independent casts with the same input dtype and FP8 format in one launch.
+hipError_t launch_quantize_pair(const QuantParams &a, const QuantParams &b, hipStream_t s);
 hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
 // 0: tile shape from the cost model; 1..4: force 256x256, 256x192, 192x256, 256x128
 void set_gemm_tile_override(int tile);

@@ -88,8 +88,22 @@ __device__ __forceinline__ void unpack16(const uint4 &v, float *f) {
   }
 }
 
+// One launch casts one tensor, or two independent ones (the forward's weight
+// refresh and input cast) whose tiles follow each other in one grid, so the
+// second tensor's tiles fill the first one's tail instead of a second launch
+// ramping up after it.
+struct QuantJob {
+  QuantParams p;
+  int64_t tiles, tiles_c;
+  int32_t aligned, pad;
+};
+struct QuantPair {
+  QuantJob j[2];
+  int32_t n, pad;
+};
+
 template <bool BF16, int FMT>
-__global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64_t tiles_c, int aligned) {
+__global__ __launch_bounds__(kThreads) void quantize_kernel(QuantPair pp) {
   __shared__ __attribute__((aligned(16))) uint8_t tile[kTile * kTile];
   __shared__ uint32_t red[kThreads / 64];
   // Phase 1 mapping: one 16-byte load per lane per step, consecutive lanes on
@@ -98,7 +112,12 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64
   constexpr int LPR = kTile / EPL;           // lanes per tile row
   constexpr int NLD = kTile * kTile / (EPL * kThreads);  // loads per lane
   const int tid = threadIdx.x;
-  const int64_t t = blockIdx.x;
+  const bool second = pp.n > 1 && int64_t(blockIdx.x) >= pp.j[0].tiles;  // uniform per workgroup
+  const QuantJob &job = second ? pp.j[1] : pp.j[0];
+  const QuantParams &p = job.p;
+  const int64_t tiles_c = job.tiles_c;
+  const int aligned = job.aligned;
+  const int64_t t = second ? int64_t(blockIdx.x) - pp.j[0].tiles : int64_t(blockIdx.x);
   const int64_t r0 = (t / tiles_c) * kTile;
   const int64_t c0 = (t % tiles_c) * kTile;
   const float scale = *p.scale;
@@ -232,28 +251,55 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantParams p, int64
 }
 
 template <bool BF16>
-hipError_t launch_fmt(const QuantParams &p, hipStream_t s, int64_t tiles, int64_t tiles_c, int aligned) {
-  if (p.fmt == 0)
-    hipLaunchKernelGGL((quantize_kernel<BF16, 0>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, p, tiles_c, aligned);
+hipError_t launch_fmt(const QuantPair &pp, int fmt, hipStream_t s) {
+  int64_t tiles = 0;
+  for (int i = 0; i < pp.n; ++i) tiles += pp.j[i].tiles;
+  if (fmt == 0)
+    hipLaunchKernelGGL((quantize_kernel<BF16, 0>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
   else
-    hipLaunchKernelGGL((quantize_kernel<BF16, 1>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, p, tiles_c, aligned);
+    hipLaunchKernelGGL((quantize_kernel<BF16, 1>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
   return hipGetLastError();
+}
+
+QuantJob make_job(const QuantParams &p) {
+  QuantJob j{};
+  j.p = p;
+  const int64_t tiles_r = (p.rows + kTile - 1) / kTile;
+  const int64_t tiles_c = (p.cols + kTile - 1) / kTile;
+  j.tiles = tiles_r * tiles_c;
+  if (j.tiles < 1) j.tiles = 1;  // still writes the scale_inv snapshot
+  j.tiles_c = tiles_c < 1 ? 1 : tiles_c;
+  const int64_t esize = p.in_bf16 ? 2 : 4;
+  const bool in_al = (reinterpret_cast<uintptr_t>(p.in) % 16 == 0) && ((p.cols * esize) % 16 == 0);
+  const bool row_al = p.q_row == nullptr || ((reinterpret_cast<uintptr_t>(p.q_row) % 16 == 0) && p.ld_row % 16 == 0);
+  const bool col_al = p.q_col == nullptr || ((reinterpret_cast<uintptr_t>(p.q_col) % 16 == 0) && p.ld_col % 16 == 0);
+  j.aligned = (in_al && row_al && col_al) ? 1 : 0;
+  return j;
+}
+
+hipError_t launch_pair(const QuantPair &pp, hipStream_t s) {
+  return pp.j[0].p.in_bf16 ? launch_fmt<true>(pp, pp.j[0].p.fmt, s) : launch_fmt<false>(pp, pp.j[0].p.fmt, s);
 }
 
 }  // namespace
 
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s) {
-  const int64_t tiles_r = (p.rows + kTile - 1) / kTile;
-  const int64_t tiles_c = (p.cols + kTile - 1) / kTile;
-  int64_t tiles = tiles_r * tiles_c;
-  if (tiles < 1) tiles = 1;  // still writes the scale_inv snapshot
-  const int64_t esize = p.in_bf16 ? 2 : 4;
-  const bool in_al = (reinterpret_cast<uintptr_t>(p.in) % 16 == 0) && ((p.cols * esize) % 16 == 0);
-  const bool row_al = p.q_row == nullptr || ((reinterpret_cast<uintptr_t>(p.q_row) % 16 == 0) && p.ld_row % 16 == 0);
-  const bool col_al = p.q_col == nullptr || ((reinterpret_cast<uintptr_t>(p.q_col) % 16 == 0) && p.ld_col % 16 == 0);
-  const int aligned = (in_al && row_al && col_al) ? 1 : 0;
-  const int64_t tc = tiles_c < 1 ? 1 : tiles_c;
-  return p.in_bf16 ? launch_fmt<true>(p, s, tiles, tc, aligned) : launch_fmt<false>(p, s, tiles, tc, aligned);
+  QuantPair pp{};
+  pp.j[0] = make_job(p);
+  pp.n = 1;
+  return launch_pair(pp, s);
+}
+
+hipError_t launch_quantize_pair(const QuantParams &a, const QuantParams &b, hipStream_t s) {
+  if (a.in_bf16 != b.in_bf16 || a.fmt != b.fmt) {  // different kernel instances: two launches
+    const hipError_t e = launch_quantize(a, s);
+    return e != hipSuccess ? e : launch_quantize(b, s);
+  }
+  QuantPair pp{};
+  pp.j[0] = make_job(a);
+  pp.j[1] = make_job(b);
+  pp.n = 2;
+  return launch_pair(pp, s);
 }
 
 }  // namespace qe

@@ -10,8 +10,10 @@ from tests.gpu_util import dev_bytes, dev_f32, torch, upload
 
 class Spec:
     def __init__(self, shapes, tokens, M, history, margin, in_dtype, shared_view, out_dtype="f32", seed=0,
-                 cfg=90, outliers=False, scaling="delayed"):
+                 cfg=90, outliers=False, scaling="delayed", w_dtype=None, fmt_w="E4M3"):
+        """`w_dtype`: the master weights' dtype (default `in_dtype`); `fmt_w`: W's FP8 format."""
         self.shapes, self.tokens, self.M = shapes, tokens, M
+        self.w_dtype, self.fmt_w = w_dtype or in_dtype, fmt_w
         self.history, self.margin, self.in_dtype = history, margin, in_dtype
         self.shared_view, self.out_dtype, self.seed, self.cfg = shared_view, out_dtype, seed, cfg
         self.outliers, self.scaling = outliers, scaling
@@ -28,7 +30,7 @@ class Spec:
 
     def weight(self, u):
         n, k = self.shapes[u]
-        return W.normal(W.rng_for(self.seed, self.cfg, u, W.ROLE_W), (n, k), 0.02, self.in_dtype)
+        return W.normal(W.rng_for(self.seed, self.cfg, u, W.ROLE_W), (n, k), 0.02, self.w_dtype)
 
     def inputs(self, u, m, step):
         n, k = self.shapes[u]
@@ -55,12 +57,13 @@ class GpuStage:
                               replay_on_caller=replay_on_caller)
         self.streams = streams
         self.n_actions = 0
-        dt = qe.BF16 if spec.in_dtype == "bf16" else qe.F32
+        dt = qe.BF16 if spec.w_dtype == "bf16" else qe.F32
+        fw = qe.E4M3 if spec.fmt_w == "E4M3" else qe.E5M2
         self.w = [upload(spec.weight(u) if weights is None else weights[u], self.d) for u in range(len(spec.shapes))]
         for u, (n, k) in enumerate(spec.shapes):
             rec = qe.SCALING_CURRENT if spec.scaling == "current" else qe.SCALING_DELAYED
             st, idx = self.ctx.qe_layer_register(0, u, n, k, spec.tokens, self.w[u], dt, spec.history, spec.margin,
-                                                 scaling=rec)
+                                                 fmt_w=fw, scaling=rec)
             assert st == "OK" and idx == u
         self.grad = torch.zeros(spec.grad_elems(), dtype=torch.float32, device=self.d)
         for u, (n, k) in enumerate(spec.shapes):
@@ -165,7 +168,8 @@ class OracleStage:
         self.st = Stage(spec.M)
         for u, (n, k) in enumerate(spec.shapes):
             w = spec.weight(u) if weights is None else weights[u]
-            self.st.add_layer(0, u, w.as_f32(), spec.tokens, spec.history, spec.margin, scaling=spec.scaling)
+            self.st.add_layer(0, u, w.as_f32(), spec.tokens, spec.history, spec.margin, fmt_w=spec.fmt_w,
+                             scaling=spec.scaling)
         self.buf = 1 << 12
         self.st.add_buffer(self.buf, spec.grad_elems())
         for u, (n, k) in enumerate(spec.shapes):
@@ -210,7 +214,7 @@ class OracleStage:
                 o = spec.offset(u, m)
                 acc += g[o:o + n * k].reshape(n, k)
             w = (self.st.layers[u].w.astype(np.float64) - lr * acc).astype(np.float32)
-            t = W.Tensor(W.f32_to_bf16_bits(w), "bf16") if spec.in_dtype == "bf16" else W.Tensor(w, "f32")
+            t = W.Tensor(W.f32_to_bf16_bits(w), "bf16") if spec.w_dtype == "bf16" else W.Tensor(w, "f32")
             new.append(t)
         return new
 

@@ -90,6 +90,16 @@ def test_ragged_layers_bf16_schedule():
     run_pair(spec, [S.SINGLE, S.SINGLE], check_codes_after=4)
 
 
+@pytest.mark.parametrize("w_dtype,fmt_w", [("f32", "E4M3"), ("bf16", "E5M2")])
+def test_weight_dtype_or_format_unlike_input(w_dtype, fmt_w):
+    """W's cast and X's cast share a launch only when they share the input dtype and FP8
+    format; here they do not (fp32 master weights under bf16 activations, or an E5M2 weight
+    code), so the refresh runs them as two launches, with the same codes and scales."""
+    spec = Spec([(200, 136), (256, 384)], tokens=100, M=2, history=4, margin=0, in_dtype="bf16",
+                shared_view=True, cfg=93, w_dtype=w_dtype, fmt_w=fmt_w)
+    run_pair(spec, [S.SINGLE] * 2, check_codes_after=4)
+
+
 def test_bf16_outputs():
     spec = Spec([(256, 384)], tokens=192, M=2, history=4, margin=0, in_dtype="bf16", shared_view=True,
                 out_dtype="bf16", cfg=92)
