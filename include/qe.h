@@ -188,7 +188,7 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
  * measured per-round cost; the others force one shape (for tests and
  * measurements).  Process-wide; it applies to launches enqueued afterwards
  * (a graph captured earlier keeps the shapes it was captured with).  The
- * four shapes give the same bits: the same 16x16x128 MFMA with the same
+ * five shapes give the same bits: the same 16x16x128 MFMA with the same
  * reduction bytes per lane, the same order along K, no split reduction.
  * Errors: QE_ERR_INVALID_ARG for a value outside the enum. */
 typedef enum {
@@ -196,7 +196,8 @@ typedef enum {
   QE_TILE_256x256 = 1,
   QE_TILE_256x192 = 2,
   QE_TILE_192x256 = 3,
-  QE_TILE_256x128 = 4
+  QE_TILE_256x128 = 4,
+  QE_TILE_256x224 = 5
 } qe_gemm_tile;
 qe_status qe_set_gemm_tile(qe_gemm_tile tile);
 

@@ -594,7 +594,7 @@ qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t row
 }
 
 qe_status qe_set_gemm_tile(qe_gemm_tile tile) {
-  if (tile < QE_TILE_AUTO || tile > QE_TILE_256x128) return QE_ERR_INVALID_ARG;
+  if (tile < QE_TILE_AUTO || tile > QE_TILE_256x224) return QE_ERR_INVALID_ARG;
   qe::set_gemm_tile_override(int(tile));
   return QE_OK;
 }

@@ -13,8 +13,8 @@
 // Two kernels share the scheme below; both use v_mfma_f32_16x16x128_f8f6f4
 // with the same assignment of reduction bytes to lanes, so every tile shape
 // accumulates each output element in the same order and gives the same bits.
-//  * gemm_tn_w4_kernel, 256 x 256 x 128 tiles (and 256 x 192, 192 x 256):
-//    four waves (one per SIMD) on a 2 x 2 grid, each a 128 x 128 sub-tile of
+//  * gemm_tn_w4_kernel, 256 x 256 x 128 tiles (and 256 x 224, 256 x 192,
+//    192 x 256): four waves (one per SIMD) on a 2 x 2 grid, each a 128 x 128 sub-tile of
 //    8 x 8 MFMA blocks.  A K tile's 64 MFMAs run in two phases; every fragment
 //    read or LDS-bound load is issued right after an MFMA, in a fixed order
 //    (sched_barrier), so the MFMA pipe stays busy in the single wave, and the
@@ -331,8 +331,8 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
   }
 }
 
-// 256 x 256 x 128 tile (also 256 x 192 and 192 x 256), four waves (one per
-// SIMD) on a 2 x 2 grid, each wave a TM x TN sub-tile of 16 x 16 blocks of
+// 256 x 256 x 128 tile (also 256 x 224, 256 x 192 and 192 x 256), four waves
+// (one per SIMD) on a 2 x 2 grid, each wave a TM x TN sub-tile of 16 x 16 blocks of
 // v_mfma_f32_16x16x128_f8f6f4, one MFMA per block per K tile.  (On random FP8
 // operands this MFMA sustains about a third more throughput than the 32 x 32 x
 // 64 one on MI355X, which draws more power per FLOP; with constant operands
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
 // the waits for fragment reads inside an iteration can then be partial.
 template <int FA, int FB, int OUT, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok) {
-  static_assert((BM == 256 || BM == 192) && (BN == 256 || BN == 192), "tile sizes");
+  static_assert((BM == 256 || BM == 192) && (BN == 256 || BN == 224 || BN == 192), "tile sizes");
   constexpr int NW = 4, TM = BM / 2, TN = BN / 2;
   constexpr int I = TM / 16, J = TN / 16;    // 16 x 16 MFMA blocks per wave sub-tile
   constexpr int IA = I / 2, IB = I - IA;     // block rows of phase A and phase B
@@ -595,7 +595,7 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   // (buffer instructions: the row offset is a scalar operand; every offset of
   // the wave's TM x TN block stays below 2^31)
   const bool fast = vec_ok && nfull && m0 + BM <= M && g.ldc * ES * (TM + 2) < (int64_t(1) << 31);
-  const bool has_col = (lane & 31) * 4 < TN;  // TN = 96: 24 of each 32 lanes hold a column quad
+  const bool has_col = (lane & 31) * 4 < TN;  // TN = 112 or 96: 28 or 24 of each 32 lanes hold a column quad
   const int wu = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t voff = uint32_t((lane >> 5) * g.ldc + (lane & 31) * 4) * uint32_t(ES);
   char *cbase = static_cast<char *>(g.c) + ((m0 + (wu >> 1) * TM) * g.ldc + n0 + (wu & 1) * TN) * ES;
@@ -743,10 +743,12 @@ hipError_t launch_fmts(const GemmParams &g, hipStream_t s) {
 // Relative cost of a round of tiles against a round of 256 x 256 ones at the
 // same K, measured on MI355X (K = 4096, one round of each shape, bf16 out):
 // 256 x 192 0.89, 192 x 256 0.86 (0.75 of the MFMA work at a lower
-// efficiency per FLOP), the 8-wave 256 x 128 kernel 0.905.  Rounded up, so a
-// tie keeps the larger tile.
+// efficiency per FLOP), the 8-wave 256 x 128 kernel 0.905; 256 x 224 0.978
+// (bf16 out) and 0.972 (FP32 out), two rounds against two.  Rounded up, so
+// a tie keeps the larger tile.
 constexpr double kCost192 = 0.90;
 constexpr double kCost128 = 0.92;
+constexpr double kCost224 = 0.98;
 
 static std::atomic<int> g_tile_override{0};
 
@@ -783,7 +785,8 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   // Tile choice by wave quantization: each CU runs one workgroup at a time, so
   // a grid costs ceil(tiles / CUs) rounds of one tile's time; the smaller tiles
   // win where the 256 x 256 grid leaves its last round mostly empty (N = 6144:
-  // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.89).
+  // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.89;
+  // N = 14336: 896 tiles = 3.5 rounds, against 1024 of 256 x 224 = 4 of 0.98).
   auto rounds = [&](int64_t bm, int64_t bn) {
     const int64_t t = ((g.m + bm - 1) / bm) * ((g.n + bn - 1) / bn);
     return double((t + kCUs - 1) / kCUs);
@@ -793,18 +796,22 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   const double c128 = kCost128 * rounds(256, 128);
   const double cn192 = kCost192 * rounds(256, 192);
   const double cm192 = kCost192 * rounds(192, 256);
+  const double cn224 = kCost224 * rounds(256, 224);
   if (force == 1) return launch_w4_fmts<256, 256>(g, s);
   if (force == 2) return launch_w4_fmts<256, 192>(g, s);
   if (force == 3) return launch_w4_fmts<192, 256>(g, s);
   if (force == 4) return launch_fmts<256, 128, 4, 2>(g, s);
+  if (force == 5) return launch_w4_fmts<256, 224>(g, s);
   double best = c256;
   int pick = 1;
+  if (cn224 < best) { best = cn224; pick = 5; }
   if (cn192 < best) { best = cn192; pick = 2; }
   if (cm192 < best) { best = cm192; pick = 3; }
   if (c128 < best) { best = c128; pick = 4; }
   if (pick == 2) return launch_w4_fmts<256, 192>(g, s);
   if (pick == 3) return launch_w4_fmts<192, 256>(g, s);
   if (pick == 4) return launch_fmts<256, 128, 4, 2>(g, s);
+  if (pick == 5) return launch_w4_fmts<256, 224>(g, s);
   return launch_w4_fmts<256, 256>(g, s);
 }
 

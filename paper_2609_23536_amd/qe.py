@@ -197,7 +197,7 @@ def qe_fp8_gemm_tn(a, fmt_a: int, lda: int, b, fmt_b: int, ldb: int, m: int, n: 
                                     ptr(b_scale_inv), ptr(c), c_dtype, ldc, mode, stream_handle(stream)))
 
 
-TILE_AUTO, TILE_256x256, TILE_256x192, TILE_192x256, TILE_256x128 = 0, 1, 2, 3, 4
+TILE_AUTO, TILE_256x256, TILE_256x192, TILE_192x256, TILE_256x128, TILE_256x224 = 0, 1, 2, 3, 4, 5
 
 
 def qe_set_gemm_tile(tile: int) -> str:

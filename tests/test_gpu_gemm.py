@@ -186,10 +186,10 @@ def _int_operands(d, m, n, k, seed):
 # full tiles of every shape, ragged edges in M, N and K, a partial last K tile,
 # and grids of several rounds
 TILE_SHAPES = [(768, 768, 256), (1000, 700, 320), (576, 4096, 384), (4096, 576, 130), (2304, 2304, 512),
-               (193, 191, 129), (4096, 6144, 256)]
+               (193, 191, 129), (4096, 6144, 256), (2048, 7168, 384)]
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3, 4], ids=["256x256", "256x192", "192x256", "256x128"])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5], ids=["256x256", "256x192", "192x256", "256x128", "256x224"])
 @pytest.mark.parametrize("shape", TILE_SHAPES, ids=lambda s: "x".join(map(str, s)))
 def test_forced_tile_shapes_exact(forced_tile, tile, shape):
     """Each macro-tile shape on integer operands: FP32 store, BF16 store and
@@ -221,10 +221,10 @@ def test_forced_tile_shapes_exact(forced_tile, tile, shape):
     assert torch.equal(ca[:, n:], base[:, n:])
 
 
-@pytest.mark.parametrize("shape", [(768, 768, 1000), (1000, 700, 320), (576, 4096, 384)], ids=str)
+@pytest.mark.parametrize("shape", [(768, 768, 1000), (1000, 700, 320), (576, 4096, 384), (1024, 1344, 640)], ids=str)
 def test_tile_shapes_same_bits(forced_tile, shape):
-    """Every macro-tile shape (256x256, 256x192, 192x256 with four waves,
-    256x128 with eight) runs the same MFMA with the same reduction bytes per
+    """Every macro-tile shape (256x256, 256x224, 256x192, 192x256 with four
+    waves, 256x128 with eight) runs the same MFMA with the same reduction bytes per
     lane in the same K order: on random codes (inexact FP32 sums) their outputs
     are bit-identical."""
     qe = forced_tile
@@ -234,7 +234,7 @@ def test_tile_shapes_same_bits(forced_tile, shape):
     A = random_codes(rng, m, k, 0, rup16(k))
     B = random_codes(rng, n, k, 1, rup16(k))
     outs = []
-    for tile in (1, 2, 3, 4):
+    for tile in (1, 2, 3, 4, 5):
         assert qe.qe_set_gemm_tile(tile) == "OK"
         outs.append(run_gemm(qe, d, A, 0, B, 1, m, n, k, 2.0 ** -2, 2.0 ** 3, qe.F32, n)[: m * n])
     ref = gemm.gemm_tn(A[:, :k], "E4M3", B[:, :k], "E5M2", 2.0 ** -2, 2.0 ** 3)

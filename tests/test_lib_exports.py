@@ -56,6 +56,6 @@ def test_invalid_args_rejected_without_device():
         == "INVALID_ARG"
     assert qe.qe_fp8_gemm_tn(16, 7, 16, 16, qe.E4M3, 16, 4, 4, 16, 16, 16, 16, qe.F32, 4, stream=0) == "INVALID_ARG"
     assert qe.qe_amax_scale_update([meta], stream=0) == "INVALID_ARG"
-    assert qe.qe_set_gemm_tile(5) == "INVALID_ARG"
+    assert qe.qe_set_gemm_tile(6) == "INVALID_ARG"
     assert qe.qe_set_gemm_tile(-1) == "INVALID_ARG"
     assert qe.qe_set_gemm_tile(qe.TILE_AUTO) == "OK"
