@@ -221,7 +221,12 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
       }
       hipGraph_t graph = nullptr;
       if (hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal) != hipSuccess) return QE_ERR_HIP;
-      const hipError_t le = enqueue(c, plan, false, c->gs);
+      hipError_t le = enqueue(c, plan, false, c->gs);
+      // The action's completion event is a node of the graph: recorded by the
+      // replay itself on the stream it runs on.  (On MI355X a separate record
+      // after the launch adds about 5 us of device time per action; the node
+      // adds none.)
+      if (le == hipSuccess) le = hipEventRecord(on_caller ? c->ev_chain : c->ev_tail, c->gs);
       const hipError_t ce = hipStreamEndCapture(c->gs, &graph);
       if (le != hipSuccess || ce != hipSuccess || graph == nullptr) {
         if (graph) (void)hipGraphDestroy(graph);
@@ -242,13 +247,12 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
     c->st.replays += 1;
   } else {
     if (enqueue(c, plan, c->timing != 0, s) != hipSuccess) return QE_ERR_HIP;
+    if (hipEventRecord(on_caller ? c->ev_chain : c->ev_tail, s) != hipSuccess) return QE_ERR_HIP;
   }
   if (on_caller) {
-    if (hipEventRecord(c->ev_chain, s) != hipSuccess) return QE_ERR_HIP;
     c->has_last = true;
     return QE_OK;
   }
-  if (hipEventRecord(c->ev_tail, c->gs) != hipSuccess) return QE_ERR_HIP;
   if (!c->cfg.one_way_handoff && caller != c->gs) {
     if (hipStreamWaitEvent(caller, c->ev_tail, 0) != hipSuccess) return QE_ERR_HIP;
   }
