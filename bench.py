@@ -94,6 +94,9 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}))
 
 
+_RESIDENT = {}  # workload -> (weights, inputs, output gradients) on the device
+
+
 class StageBench:
     def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False, current=False,
                  replay_on_caller=False):
@@ -111,12 +114,21 @@ class StageBench:
             a = t.data.view(np.int16) if bf else t.data
             return torch.from_numpy(a).to(device)
 
-        self.w, self.x, self.dy, self.y, self.dx = [], [], [], [], []
+        # the seeded weights and inputs are generated on the host once per
+        # workload and shared by every pass (the library only reads them)
+        key = (wl.key, str(device))
+        if key not in _RESIDENT:
+            ws, xs, dys = [], [], []
+            for u in range(len(wl.linears)):
+                ws.append(up(W.layer_weight(wl, u)))
+                inp = W.layer_inputs(wl, u)
+                xs.append(up(inp["x"]))
+                dys.append(up(inp["dy"]))
+            _RESIDENT.clear()
+            _RESIDENT[key] = (ws, xs, dys)
+        ws, xs, dys = _RESIDENT[key]
+        self.w, self.x, self.dy, self.y, self.dx = list(ws), list(xs), list(dys), [], []
         for u, lin in enumerate(wl.linears):
-            self.w.append(up(W.layer_weight(wl, u)))
-            inp = W.layer_inputs(wl, u)
-            self.x.append(up(inp["x"]))
-            self.dy.append(up(inp["dy"]))
             self.y.append(torch.empty((wl.tokens, lin.n_out), dtype=tdt, device=device))
             self.dx.append(torch.empty((wl.tokens, lin.k_in), dtype=tdt, device=device))
             st, idx = self.ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, wl.tokens, self.w[u], self.dt,
@@ -333,6 +345,11 @@ def cpu_baseline(wl, tokens, min_seconds=10.0):
                       f"float64 oracle, {el:.2f} s"}
 
 
+def progress(msg):
+    """One line per finished pass on stderr (stdout carries only the JSON result line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -370,6 +387,7 @@ def main():
     flops = wl.gemm_flops_per_pass()
     ms = el / args.steps * 1e3
     value = flops / (el / args.steps) / 1e12
+    progress(f"timed pass: {ms:.4f} ms per step ({wl.key})")
 
     # quiescent checkpoint at this optimizer boundary, restart into a fresh context
     ckpt = None
@@ -395,6 +413,7 @@ def main():
         torch.cuda.synchronize()
         first_ms = (time.perf_counter() - t0) * 1e3
         after_ms = timed_ms(r, torch, 0, 3)
+        progress("checkpoint / restart pass")
         assert r.ctx.qe_sync() == "OK"
         rst = r.ctx.qe_get_state()
         assert rst["device_token"] == rst["token"] and rst["e_w"] == epoch + 4
@@ -411,6 +430,7 @@ def main():
     if not args.no_ablation:
         c = StageBench(qe, torch, wl, use_graphs, dev, copy_gradients=True, replay_on_caller=on_caller)
         copied_ms = timed_ms(c, torch, args.warmup, args.steps)
+        progress("copied-gradient pass")
         c.ctx.close()
         del c
         torch.cuda.empty_cache()
@@ -420,6 +440,7 @@ def main():
     if not args.no_current:
         c = StageBench(qe, torch, wl, use_graphs, dev, current=True, replay_on_caller=on_caller)
         current_ms = timed_ms(c, torch, args.warmup, args.steps)
+        progress("current-scaling pass")
         assert c.ctx.qe_sync() == "OK"
         cst = c.ctx.qe_get_state()
         assert cst["device_token"] == cst["token"]
@@ -433,6 +454,7 @@ def main():
     if not args.no_executor:
         c = StageBench(qe, torch, wl, use_graphs, dev, replay_on_caller=not on_caller)
         other_ms = timed_ms(c, torch, args.warmup, args.steps)
+        progress("other-executor pass")
         assert c.ctx.qe_sync() == "OK"
         cst = c.ctx.qe_get_state()
         assert cst["device_token"] == cst["token"] and (cst["handoffs"] == 0) == (not on_caller)
@@ -442,6 +464,7 @@ def main():
 
     latency = None if args.no_latency else per_action_latency(qe, torch, dev)
     wgrad = None if args.no_wgrad else wgrad_place(qe, torch, dev)
+    progress("latency and dW-placement legs")
     torch.cuda.empty_cache()
 
     # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
@@ -460,17 +483,20 @@ def main():
         return t
 
     kt = instrumented(False)
+    progress("instrumented pass")
     gemm_ms, gemm_n = kt[qe.KC_GEMM]
     q_ms, q_n = kt[qe.KC_QUANT]
     u_ms, u_n = kt[qe.KC_UPDATE]
     assert kt[qe.KC_COPY][1] == 0, "direct placement launched a gradient copy"
     if copied_ms is not None:
         c_ms, c_n = instrumented(copy_gradients=True)[qe.KC_COPY]
+        progress("instrumented copied-gradient pass")
         # INIT placement (one microbatch): the copy reads the private FP32 dW and writes the view
         copy_bytes = sum(8 * lin.n_out * lin.k_in for lin in wl.linears)
         copy_gbs = copy_bytes * args.steps / (c_ms * 1e-3) / 1e9
     if current_ms is not None:
         kc = instrumented(current=True)
+        progress("instrumented current-scaling pass")
         a_ms, a_n = kc[qe.KC_AMAX]
         cq_ms, cq_n = kc[qe.KC_QUANT]
         a_gbs = amax_bytes(wl) * args.steps / (a_ms * 1e-3) / 1e9
@@ -528,6 +554,7 @@ def main():
         out["wgrad_place"] = wgrad
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+        progress("cpu baseline")
     print(json.dumps(out), flush=True)
 
 
