@@ -18,7 +18,13 @@ per second over the whole step, quantization and scale updates included.
 `roofline` is the GEMM kernel alone, timed with HIP events on the stream the
 library launches it on, in an instrumented eager pass over the same steps.
 `cpu_baseline` times the CPU oracle on a bounded sample (the stage's linears
-in order, at full token count, until at least 10 s of CPU work).
+in order, at full token count, until at least 10 s of CPU work).  Beside the
+headline the line carries the same steps under the other executor, with the
+actions' kernels launched the other way (direct launches against graph
+replay), with copied gradients, with current scaling and after a checkpoint
+restart; per-action latencies of a single small linear; and the deferred dW
+GEMM alone at the zero-bubble microbatch, INIT- and ACCUM-placed.  One
+progress line per finished pass goes to stderr.
 """
 from __future__ import annotations
 
@@ -52,6 +58,9 @@ def parse():
                     help="caller: every action replayed on the caller's stream (stream order is the handoff); "
                          "two-way: on the library's graph stream behind the paper's two-way handoff")
     ap.add_argument("--no-executor", action="store_true", help="skip the pass with the other executor")
+    ap.add_argument("--no-launch-mode", action="store_true",
+                    help="skip the pass that launches the same actions the other way (direct launches under graph "
+                         "replay, graph replay under --eager)")
     ap.add_argument("--no-wgrad", action="store_true",
                     help="skip the dW-placement measurement at the zero-bubble workload's 2048-token microbatch")
     ap.add_argument("--no-latency", action="store_true",
@@ -230,55 +239,63 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
 def wgrad_place(qe, torch, device, tokens=2048, reps=20):
     """The deferred dW GEMM with direct placement at the zero-bubble workload's
     microbatch (2048 tokens) and the Llama-3-8B stage's four linears: dW =
-    dY^T X from the transposed E5M2 / E4M3 codes, INIT-placed into [N, K] views
-    of one flat FP32 buffer (each view at its own offset, as per microbatch).
-    Algorithmic bytes per launch: (N + K) * tokens code bytes read + 4 N K
-    written; roofline time max(FLOPs / MFMA peak, bytes / HBM peak)."""
+    dY^T X from the transposed E5M2 / E4M3 codes, placed into [N, K] views of
+    one flat FP32 buffer (each view at its own offset, as per microbatch):
+    INIT (the headline figures) and ACCUM (read-add-write, as when microbatches
+    share one view).  Algorithmic bytes per launch: (N + K) * tokens code bytes
+    read + 4 N K written (INIT) or 8 N K read and written (ACCUM); roofline time
+    max(FLOPs / MFMA peak, bytes / HBM peak)."""
     import workloads as W
     wl = W.WORKLOADS["llama3_8b_zb_8x2048"]
     assert wl.tokens == tokens
     one = torch.ones(1, device=device)
     offs = wl.grad_offsets()
-    grad = torch.empty(wl.flat_grad_elems(), dtype=torch.float32, device=device)
-    tot_t = tot_b = tot_f = tot_roof = 0.0
-    per = []
-    for u, lin in enumerate(wl.linears):
-        n, k = lin.n_out, lin.k_in
-        g = torch.Generator(device=device)
-        g.manual_seed(u)
-        a = (torch.randn(n, tokens, device=device, generator=g) * 0.5).to(torch.float8_e5m2).view(torch.uint8)
-        b = (torch.randn(k, tokens, device=device, generator=g) * 0.5).to(torch.float8_e4m3fn).view(torch.uint8)
-        view = grad[offs[u]:]
+    grad = torch.zeros(wl.flat_grad_elems(), dtype=torch.float32, device=device)
+    res = {}
+    for mode, out_bytes in ((qe.INIT, 4), (qe.ACCUM, 8)):
+        tot_t = tot_b = tot_f = tot_roof = 0.0
+        per = []
+        for u, lin in enumerate(wl.linears):
+            n, k = lin.n_out, lin.k_in
+            g = torch.Generator(device=device)
+            g.manual_seed(u)
+            a = (torch.randn(n, tokens, device=device, generator=g) * 0.5).to(torch.float8_e5m2).view(torch.uint8)
+            b = (torch.randn(k, tokens, device=device, generator=g) * 0.5).to(torch.float8_e4m3fn).view(torch.uint8)
+            view = grad[offs[u]:]
 
-        def run():
-            st = qe.qe_fp8_gemm_tn(a, qe.E5M2, tokens, b, qe.E4M3, tokens, n, k, tokens, one, one, view, qe.F32, k,
-                                   qe.INIT)
-            assert st == "OK", st
+            def run():
+                st = qe.qe_fp8_gemm_tn(a, qe.E5M2, tokens, b, qe.E4M3, tokens, n, k, tokens, one, one, view, qe.F32,
+                                       k, mode)
+                assert st == "OK", st
 
-        for _ in range(3):
-            run()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            run()
-        e1.record()
-        e1.synchronize()
-        t = e0.elapsed_time(e1) / reps * 1e-3
-        byts = (n + k) * tokens + 4 * n * k
-        flop = 2.0 * n * k * tokens
-        roof = max(flop / (FP8_PEAK_TFLOPS * 1e12), byts / (HBM_PEAK_GBS * 1e9))
-        per.append({"linear": lin.name, "n": n, "k": k, "us": round(t * 1e6, 2), "gbs": round(byts / t / 1e9, 1),
-                    "tflops": round(flop / t / 1e12, 1), "roofline_frac": round(roof / t, 4),
-                    "bound": "hbm" if byts / (HBM_PEAK_GBS * 1e9) > flop / (FP8_PEAK_TFLOPS * 1e12) else "mfma"})
-        tot_t += t
-        tot_b += byts
-        tot_f += flop
-        tot_roof += roof
-    return {"workload": wl.key, "tokens": tokens, "placement": "INIT into per-view offsets of one flat FP32 buffer",
-            "achieved_gbs": round(tot_b / tot_t / 1e9, 1), "unit": "GB/s", "peak_gbs": HBM_PEAK_GBS,
-            "frac_hbm": round(tot_b / tot_t / 1e9 / HBM_PEAK_GBS, 4), "tflops": round(tot_f / tot_t / 1e12, 1),
-            "roofline_frac": round(tot_roof / tot_t, 4), "per_linear": per}
+            for _ in range(3):
+                run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                run()
+            e1.record()
+            e1.synchronize()
+            t = e0.elapsed_time(e1) / reps * 1e-3
+            byts = (n + k) * tokens + out_bytes * n * k
+            flop = 2.0 * n * k * tokens
+            roof = max(flop / (FP8_PEAK_TFLOPS * 1e12), byts / (HBM_PEAK_GBS * 1e9))
+            per.append({"linear": lin.name, "n": n, "k": k, "us": round(t * 1e6, 2), "gbs": round(byts / t / 1e9, 1),
+                        "tflops": round(flop / t / 1e12, 1), "roofline_frac": round(roof / t, 4),
+                        "bound": "hbm" if byts / (HBM_PEAK_GBS * 1e9) > flop / (FP8_PEAK_TFLOPS * 1e12) else "mfma"})
+            tot_t += t
+            tot_b += byts
+            tot_f += flop
+            tot_roof += roof
+        res[mode] = {"achieved_gbs": round(tot_b / tot_t / 1e9, 1), "unit": "GB/s", "peak_gbs": HBM_PEAK_GBS,
+                     "frac_hbm": round(tot_b / tot_t / 1e9 / HBM_PEAK_GBS, 4), "tflops": round(tot_f / tot_t / 1e12, 1),
+                     "roofline_frac": round(tot_roof / tot_t, 4), "per_linear": per}
+    out = {"workload": wl.key, "tokens": tokens, "placement": "INIT into per-view offsets of one flat FP32 buffer"}
+    out.update(res[qe.INIT])
+    acc = res[qe.ACCUM]
+    out["accumulate"] = {"placement": "ACCUM (read-add-write) into the same views", **acc}
+    return out
 
 
 def timed_ms(b, torch, warmup, steps):
@@ -462,6 +479,18 @@ def main():
         del c
         torch.cuda.empty_cache()
 
+    # the same steps with the actions' kernels launched the other way (direct
+    # launches when the headline replays graphs), on the same executor
+    mode_ms = None
+    if not args.no_launch_mode:
+        c = StageBench(qe, torch, wl, not use_graphs, dev, replay_on_caller=on_caller)
+        mode_ms = timed_ms(c, torch, args.warmup, args.steps)
+        assert c.ctx.qe_sync() == "OK"
+        c.ctx.close()
+        del c
+        torch.cuda.empty_cache()
+        progress("other launch-mode pass")
+
     latency = None if args.no_latency else per_action_latency(qe, torch, dev)
     wgrad = None if args.no_wgrad else wgrad_place(qe, torch, dev)
     progress("latency and dW-placement legs")
@@ -548,6 +577,10 @@ def main():
             "ms_per_step": round(other_ms, 4), "value": round(flops / (other_ms * 1e-3) / 1e12, 2),
             "unit": "TFLOP/s", "step_time_vs_headline": round(other_ms / ms, 4),
             "handoffs_per_step": 2 * 3 * wl.microbatches * len(wl.linears) if on_caller else 0}
+    if mode_ms is not None:
+        out["launch_mode_" + ("direct" if use_graphs else "graph_replay")] = {
+            "ms_per_step": round(mode_ms, 4), "value": round(flops / (mode_ms * 1e-3) / 1e12, 2),
+            "unit": "TFLOP/s", "step_time_vs_headline": round(mode_ms / ms, 4)}
     if latency is not None:
         out["per_action_latency"] = latency
     if wgrad is not None:
