@@ -47,10 +47,13 @@ class Spec:
 
 class GpuStage:
     def __init__(self, qe, spec, use_graphs=False, device=None, copy_gradients=False, weights=None,
-                 replay_on_caller=False, streams=None):
+                 replay_on_caller=False, streams=None, x_misaligned=False):
         """`weights`: the current master weights (workloads.Tensor per layer), default the initial ones.
         `streams`: caller streams used in turn, one per action (inputs are uploaded and outputs
-        allocated on the action's stream); default torch's current stream."""
+        allocated on the action's stream); default torch's current stream.
+        `x_misaligned`: hand F its input one element past a 16-byte boundary (so the cast of X
+        takes the unaligned path while W's stays aligned)."""
+        self.x_misaligned = x_misaligned
         self.qe, self.spec = qe, spec
         self.d = device
         self.ctx = qe.Context(spec.M, use_graphs=use_graphs, copy_gradients=copy_gradients,
@@ -102,8 +105,14 @@ class GpuStage:
         x, dy = spec.inputs(u, m, step)
         if a == "F":
             y = self._out(spec.tokens, n)
-            st, self.refs[(u, m)] = self.ctx.qe_fp8_linear_fwd(u, key, upload(x, self.d), dt, spec.tokens,
-                                                               y, odt, caller=caller)
+            xin = upload(x, self.d)
+            if self.x_misaligned:
+                buf = torch.empty(xin.numel() + 1, dtype=xin.dtype, device=self.d)
+                buf[1:].copy_(xin.reshape(-1))
+                xin = buf[1:].view(xin.shape)
+                assert xin.data_ptr() % 16 != 0
+            st, self.refs[(u, m)] = self.ctx.qe_fp8_linear_fwd(u, key, xin, dt, spec.tokens, y, odt, caller=caller)
+            self.written_x = xin  # keep the offset buffer alive until the action has run
             self.outs[("y", u, m, step)] = y
         elif a == "dI":
             dx = self._out(spec.tokens, k)

@@ -40,10 +40,10 @@ def compare_outputs(g, o, tol=1e-3):
         assert rel_err(got, ref) <= tol, key
 
 
-def run_pair(spec, steps, use_graphs=False, check_codes_after=None):
+def run_pair(spec, steps, use_graphs=False, check_codes_after=None, **stage_kw):
     qe = need_lib()
     d = dev()
-    g = GpuStage(qe, spec, use_graphs=use_graphs, device=d)
+    g = GpuStage(qe, spec, use_graphs=use_graphs, device=d, **stage_kw)
     o = OracleStage(spec)
     for step, sched in enumerate(steps):
         S.check_legal(sched, spec.M)
@@ -98,6 +98,16 @@ def test_weight_dtype_or_format_unlike_input(w_dtype, fmt_w):
     spec = Spec([(200, 136), (256, 384)], tokens=100, M=2, history=4, margin=0, in_dtype="bf16",
                 shared_view=True, cfg=93, w_dtype=w_dtype, fmt_w=fmt_w)
     run_pair(spec, [S.SINGLE] * 2, check_codes_after=4)
+
+
+@pytest.mark.parametrize("use_graphs", [False, True])
+def test_refresh_cast_pair_with_misaligned_input(use_graphs):
+    """The refreshing forward casts W and X in one launch; with X handed over one element past
+    a 16-byte boundary its tiles take the unaligned path and W's the aligned one, in the same
+    grid: codes, histories and scales still equal the oracle's bit for bit."""
+    spec = Spec([(256, 384), (200, 136)], tokens=192, M=2, history=4, margin=0, in_dtype="bf16",
+                shared_view=True, cfg=94)
+    run_pair(spec, [S.SINGLE] * 2, use_graphs=use_graphs, check_codes_after=4, x_misaligned=True)
 
 
 def test_bf16_outputs():
