@@ -226,8 +226,24 @@ typedef struct {
                               already satisfied).  No caller stream handle is kept between actions.
                               The same ordering contract, without the two cross-stream waits per
                               action of the graph-stream executor. */
-  int32_t reserved;
+  int32_t graph_inputs;     /* how a replayed graph meets the buffers of each call (§4.4, dynamic
+                              inputs); use_graphs only.  QE_GRAPH_INPUTS_REBIND (0, default): the
+                              graph's kernel nodes are rewritten in place with the call's pointers
+                              when they differ from the ones it holds (the host first waits for that
+                              graph's previous replay to finish); a different launch shape (token
+                              count, dtype, alignment class) captures it again.
+                              QE_GRAPH_INPUTS_RECAPTURE (1): captured again on any change.
+                              QE_GRAPH_INPUTS_COPY (2): the paper's scheme: graphs bind static
+                              library buffers (max_tokens rows of FP32 for X, Y, dY, dX per layer);
+                              each call copies X (F) or dY (dI) in after the caller -> graph edge
+                              and Y or dX out before the completion event. */
 } qe_config;
+
+enum {
+  QE_GRAPH_INPUTS_REBIND = 0,
+  QE_GRAPH_INPUTS_RECAPTURE = 1,
+  QE_GRAPH_INPUTS_COPY = 2
+};
 
 typedef struct {
   uint32_t stage, unit;  /* with microbatch/epoch/invocation, forms the TapeKey of every action */
@@ -323,6 +339,27 @@ qe_status qe_fp8_linear_bwd_full(qe_ctx *ctx, int32_t layer, qe_tape_key key, qe
 qe_status qe_arena_bind(qe_ctx *ctx, int32_t layer, uint32_t microbatch, float *buf, int64_t buf_elems,
                         int64_t offset, int64_t ld);
 
+/* Static binding (§4.3, eq. G_r = 3 M L_r): capture, before the first step,
+ * the graph of every action the stage will replay: for each registered layer
+ * and each microbatch m < M, F (m = 0 with the weight-cache refresh, since
+ * microbatch 0 is the first forward after every commit), dI, and dW into the
+ * view bound to (layer, m) (QE_PLACE_ACCUM when an earlier microbatch's view
+ * of the layer starts at the same address, else QE_PLACE_INIT; unbound
+ * (layer, m) pairs get no dW graph).  The graphs are built for `tokens` rows
+ * (0: each layer's max_tokens) and the given dtypes; the caller's X, Y, dY, dX
+ * buffers are not known yet, so every call binds them into its graph
+ * (qe_config.graph_inputs) without a new capture when the tokens and dtypes
+ * match.  Capture and instantiation time is added to qe_ctx_state.capture_ns
+ * and prebuild_ns, the graphs to .captures.  Requires use_graphs.  No device
+ * work is enqueued.  Errors: QE_ERR_INVALID_ARG (no graphs, a bad dtype,
+ * tokens above a layer's max_tokens); QE_ERR_HIP. */
+typedef struct {
+  int64_t tokens;
+  int32_t x_dtype, y_dtype;   /* qe_dtype of F's input and output */
+  int32_t dy_dtype, dx_dtype; /* qe_dtype of dI's input and output */
+} qe_prebuild_desc;
+qe_status qe_prebuild_graphs(qe_ctx *ctx, const qe_prebuild_desc *desc_host);
+
 /* Every bound view written exactly once this epoch (QE_ERR_INCOMPLETE),
  * arena valid (QE_ERR_ARENA_INVALID). */
 qe_status qe_arena_finalize(qe_ctx *ctx);
@@ -388,12 +425,15 @@ typedef struct {
   int64_t device_token;      /* last value read back by qe_sync (-1 if never) */
   int32_t arena_valid, finalized;
   int64_t graphs;            /* graph executables held */
-  int64_t captures;          /* captures performed (incl. re-captures after a pointer change) */
+  int64_t captures;          /* captures performed (prebuilt ones, first uses and re-captures) */
   int64_t replays;           /* graph launches */
   int64_t handoffs;          /* caller<->graph stream handoffs (2 per action; 0 with replay_on_caller) */
   int64_t capture_ns;        /* host time spent capturing + instantiating */
   int64_t arena_bytes;       /* bytes covered by bound views */
   int64_t device_bytes;      /* bytes the library allocated */
+  int64_t rebinds;           /* replays whose graph had kernel-node arguments rewritten first */
+  int64_t rebound_nodes;     /* kernel nodes rewritten by those rebinds */
+  int64_t prebuild_ns;       /* host time of qe_prebuild_graphs (captures + instantiations) */
 } qe_ctx_state;
 
 typedef struct {

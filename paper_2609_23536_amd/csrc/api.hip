@@ -5,12 +5,27 @@
 // Executor (§4.4 of the paper): every layer action runs on one context-owned
 // graph stream.  The graph stream first waits on the caller's stream; the
 // action's kernel sequence is then either launched directly (eager) or
-// replayed from a graph captured once per (layer, action, slot); finally an
-// event recorded at the tail is waited on by the caller's stream (the two-way
-// handoff of §2.3).  Captured graphs bind the caller's buffers directly: when
-// an action is called with different pointers or sizes than at capture time,
-// its graph is captured again (counted in qe_ctx_state.captures), so no
-// dynamic-input copy is ever needed.
+// replayed from a graph captured once per (layer, action, slot) (§4.3, eq.
+// G_r: G = 3 M L graphs, which qe_prebuild_graphs captures up front); finally
+// an event recorded right after the launch is waited on by the caller's
+// stream (the two-way handoff of §2.3).  The completion event is recorded by
+// hipEventRecord after hipGraphLaunch, never as an event-record node inside
+// the graph: on this runtime a stream waiting on an event that a graph node
+// records was measured not to wait for the graph's kernels (a consumer on the
+// caller's stream saw stale output in most trials), while a record enqueued
+// after the launch orders correctly.
+//
+// Dynamic inputs (§4.4).  Graphs bind the buffers of the call they were
+// captured for.  When an action is called with other buffers, the default
+// (QE_GRAPH_INPUTS_REBIND) rewrites the arguments of the graph's kernel nodes
+// in place (hipGraphExecKernelNodeSetParams): every action's launches are
+// recorded on the host first (qe::klaunch in record mode) and compared with
+// the ones the graph holds, and only nodes whose argument bytes differ are
+// rewritten; a different launch shape (grid, kernel instance) captures the
+// graph again.  QE_GRAPH_INPUTS_COPY is the paper's scheme: graphs bind
+// library-owned static buffers, and the caller's inputs are copied in before
+// the replay and the outputs copied out after it.  QE_GRAPH_INPUTS_RECAPTURE
+// captures the graph again on any change (for comparison).
 #include <hip/hip_runtime.h>
 #include <string.h>
 
@@ -66,10 +81,6 @@ struct Call {
 };
 using Plan = std::vector<Call>;
 
-bool same_plan(const Plan &a, const Plan &b) {
-  return a.size() == b.size() && (a.empty() || memcmp(a.data(), b.data(), a.size() * sizeof(Call)) == 0);
-}
-
 struct SlotDev {
   uint8_t *x_q_t = nullptr;   // [K, ld_t]
   uint8_t *dy_q_t = nullptr;  // [N, ld_t]
@@ -84,6 +95,9 @@ struct LayerDev {
   uint8_t *w_q = nullptr, *w_q_t = nullptr;
   float *w_sinv = nullptr;
   uint8_t *x_q = nullptr, *dy_q = nullptr;  // row-wise scratch
+  // QE_GRAPH_INPUTS_COPY only: static input / output buffers the graphs bind,
+  // sized for max_tokens rows of FP32
+  void *x_st = nullptr, *y_st = nullptr, *dy_st = nullptr, *dx_st = nullptr;
   float *grad_stage = nullptr;              // [N, K] FP32, copied-gradient path only
   int64_t ld_wq = 0, ld_wqt = 0, ld_xq = 0, ld_dyq = 0, ld_t = 0;
   std::vector<SlotDev> slots;
@@ -104,8 +118,20 @@ struct LayerDev {
 };
 
 struct GraphEntry {
+  hipGraph_t graph = nullptr;  // kept: its kernel nodes name the nodes of exec
   hipGraphExec_t exec = nullptr;
-  Plan plan;
+  hipEvent_t done = nullptr;   // recorded on the launch stream right after every replay
+  std::vector<qe::KernelRec> recs;    // the graph's launches as currently bound
+  std::vector<hipGraphNode_t> nodes;  // its kernel nodes, in launch order
+  bool rebindable = false;            // nodes match recs one to one
+  bool launched = false;
+};
+
+// A device-to-device copy around a replay (QE_GRAPH_INPUTS_COPY).
+struct Copy {
+  void *dst;
+  const void *src;
+  size_t bytes;
 };
 
 struct TimedCall {
@@ -125,7 +151,14 @@ struct qe_ctx {
   // the caller is kept, so a caller may destroy its streams between actions)
   bool has_last = false;
   hipEvent_t ev_chain = nullptr;
+  // completion event of the last action: its graph's own event, or ev_chain /
+  // ev_tail after direct launches
+  hipEvent_t last_ev = nullptr;
   long long *d_token = nullptr;
+  // qe_prebuild_graphs: the buffer every prebuilt graph binds in place of the
+  // caller's X, Y, dY and dX until a call binds its own (so a graph is never
+  // replayed on pointers that name no allocation)
+  void *placeholder = nullptr;
   std::vector<LayerDev> layers;
   std::map<uint64_t, GraphEntry> graphs;
   qe_ctx_state st{};
@@ -189,15 +222,156 @@ hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed, hipStream_t s) {
 // precede it in the chained order).
 hipError_t sync_actions(qe_ctx *c) {
   hipError_t e = hipStreamSynchronize(c->gs);
-  if (e == hipSuccess && c->has_last) e = hipEventSynchronize(c->ev_chain);
+  if (e == hipSuccess && c->has_last && c->last_ev) e = hipEventSynchronize(c->last_ev);
   return e;
 }
 
-// One action's kernel sequence, captured once per (layer, action, slot) and
-// replayed, or launched directly.  Graph-stream executor: the two-way handoff
-// around it (§2.3, §4.4).  replay_on_caller: launched on the caller's stream,
-// chained to the previous action through ev_chain.
-qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller) {
+}  // namespace
+namespace qe {
+thread_local std::vector<KernelRec> *tl_record = nullptr;
+}
+namespace {
+
+// The launches `plan` makes, recorded on the host without touching the device.
+std::vector<qe::KernelRec> record_plan(qe_ctx *c, const Plan &plan) {
+  std::vector<qe::KernelRec> v;
+  qe::tl_record = &v;
+  (void)enqueue(c, plan, false, nullptr);
+  qe::tl_record = nullptr;
+  return v;
+}
+
+// Kernel nodes of a graph captured from one stream, in launch order: such a
+// capture is a chain.  False if the graph is not a chain.
+bool chain_kernel_nodes(hipGraph_t g, std::vector<hipGraphNode_t> &out) {
+  out.clear();
+  size_t n = 0, nr = 0;
+  if (hipGraphGetNodes(g, nullptr, &n) != hipSuccess || n == 0) return false;
+  if (hipGraphGetRootNodes(g, nullptr, &nr) != hipSuccess || nr != 1) return false;
+  hipGraphNode_t cur = nullptr;
+  if (hipGraphGetRootNodes(g, &cur, &nr) != hipSuccess) return false;
+  for (size_t seen = 1; seen <= n; ++seen) {
+    hipGraphNodeType t;
+    if (hipGraphNodeGetType(cur, &t) != hipSuccess) return false;
+    if (t == hipGraphNodeTypeKernel) out.push_back(cur);
+    size_t nd = 0;
+    if (hipGraphNodeGetDependentNodes(cur, nullptr, &nd) != hipSuccess || nd > 1) return false;
+    if (nd == 0) return seen == n;
+    if (hipGraphNodeGetDependentNodes(cur, &cur, &nd) != hipSuccess) return false;
+  }
+  return false;
+}
+
+hipKernelNodeParams node_params(const qe::KernelRec &r, void **argv) {
+  hipKernelNodeParams kp;
+  memset(&kp, 0, sizeof(kp));
+  r.argv(argv);
+  kp.func = const_cast<void *>(r.func);
+  kp.gridDim = r.grid;
+  kp.blockDim = r.block;
+  kp.sharedMemBytes = r.shmem;
+  kp.kernelParams = argv;
+  kp.extra = nullptr;
+  return kp;
+}
+
+// Capture `plan` into e (replacing what e held).
+qe_status capture(qe_ctx *c, GraphEntry &e, const Plan &plan, std::vector<qe::KernelRec> &&recs) {
+  const auto t0 = std::chrono::steady_clock::now();
+  if (e.exec != nullptr) (void)hipGraphExecDestroy(e.exec);
+  if (e.graph != nullptr) (void)hipGraphDestroy(e.graph);
+  e.exec = nullptr;
+  e.graph = nullptr;
+  e.rebindable = false;
+  e.launched = false;
+  e.nodes.clear();
+  if (e.done == nullptr && hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess) {
+    e.done = nullptr;
+    return QE_ERR_HIP;
+  }
+  hipGraph_t graph = nullptr;
+  if (hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal) != hipSuccess) return QE_ERR_HIP;
+  const hipError_t le = enqueue(c, plan, false, c->gs);
+  const hipError_t ce = hipStreamEndCapture(c->gs, &graph);
+  if (le != hipSuccess || ce != hipSuccess || graph == nullptr) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return QE_ERR_HIP;
+  }
+  if (hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0) != hipSuccess) {
+    e.exec = nullptr;
+    (void)hipGraphDestroy(graph);
+    return QE_ERR_HIP;
+  }
+  e.graph = graph;
+  e.recs = std::move(recs);
+  // The nodes can be rewritten in place only if they are the recorded
+  // launches, one to one and in order.
+  bool ok = chain_kernel_nodes(graph, e.nodes) && e.nodes.size() == e.recs.size();
+  for (size_t i = 0; ok && i < e.nodes.size(); ++i) {
+    hipKernelNodeParams kp;
+    memset(&kp, 0, sizeof(kp));
+    const qe::KernelRec &r = e.recs[i];
+    ok = hipGraphKernelNodeGetParams(e.nodes[i], &kp) == hipSuccess && kp.func == r.func &&
+         kp.gridDim.x == r.grid.x && kp.gridDim.y == r.grid.y && kp.gridDim.z == r.grid.z &&
+         kp.blockDim.x == r.block.x && kp.blockDim.y == r.block.y && kp.blockDim.z == r.block.z &&
+         kp.sharedMemBytes == r.shmem;
+  }
+  e.rebindable = ok;
+  c->st.captures += 1;
+  c->st.capture_ns +=
+      std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
+  return QE_OK;
+}
+
+// Bring e's graph to `plan`: nothing if it already matches, the changed
+// kernel-node arguments rewritten in place if only arguments differ (the
+// graph's previous replay is waited for first, so no replay in flight sees a
+// half-written node), else a new capture.
+qe_status bind_graph(qe_ctx *c, GraphEntry &e, const Plan &plan) {
+  std::vector<qe::KernelRec> recs = record_plan(c, plan);
+  const int mode = c->cfg.graph_inputs;
+  bool same_shape = e.exec != nullptr && e.recs.size() == recs.size();
+  for (size_t i = 0; same_shape && i < recs.size(); ++i) same_shape = recs[i].same_shape(e.recs[i]);
+  if (!same_shape) return capture(c, e, plan, std::move(recs));
+  std::vector<size_t> diff;
+  for (size_t i = 0; i < recs.size(); ++i)
+    if (!recs[i].same_args(e.recs[i])) diff.push_back(i);
+  if (diff.empty()) return QE_OK;
+  if (mode != QE_GRAPH_INPUTS_REBIND || !e.rebindable) return capture(c, e, plan, std::move(recs));
+  if (e.launched && hipEventSynchronize(e.done) != hipSuccess) return QE_ERR_HIP;
+  for (size_t i : diff) {
+    void *argv[qe::kMaxKernelArgs];
+    const hipKernelNodeParams kp = node_params(recs[i], argv);
+    if (hipGraphExecKernelNodeSetParams(e.exec, e.nodes[i], &kp) != hipSuccess) {
+      // the exec may hold a mix of old and new arguments: never replay it
+      (void)hipGraphExecDestroy(e.exec);
+      e.exec = nullptr;
+      return QE_ERR_HIP;
+    }
+    e.recs[i] = recs[i];
+  }
+  c->st.rebinds += 1;
+  c->st.rebound_nodes += int64_t(diff.size());
+  return QE_OK;
+}
+
+hipError_t copy_all(const std::vector<Copy> &cs, hipStream_t s) {
+  for (const Copy &k : cs)
+    if (k.bytes > 0) {
+      const hipError_t e = hipMemcpyAsync(k.dst, k.src, k.bytes, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return e;
+    }
+  return hipSuccess;
+}
+
+// One action's kernel sequence, replayed from its graph (one per (layer,
+// action, slot)), or launched directly.  Graph-stream executor: the two-way
+// handoff around it (§2.3, §4.4).  replay_on_caller: launched on the caller's
+// stream, chained to the previous action through that action's completion
+// event.  `pre` / `post`: the dynamic-input copies of QE_GRAPH_INPUTS_COPY,
+// enqueued after the caller -> graph edge and before the completion event.
+qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t caller, const std::vector<Copy> &pre = {},
+                   const std::vector<Copy> &post = {}) {
   DeviceGuard dg(c->cfg.device);
   if (!dg.ok) return QE_ERR_HIP;
   const bool on_caller = c->cfg.replay_on_caller != 0;
@@ -206,55 +380,31 @@ qe_status run_plan(qe_ctx *c, const Plan &plan, uint64_t gkey, hipStream_t calle
     // Stream order covers both directions of the handoff.  The wait on the
     // previous action's event orders actions issued from different streams;
     // on the same stream it is already satisfied by stream order.
-    if (c->has_last && hipStreamWaitEvent(caller, c->ev_chain, 0) != hipSuccess) return QE_ERR_HIP;
+    if (c->has_last && hipStreamWaitEvent(caller, c->last_ev, 0) != hipSuccess) return QE_ERR_HIP;
   } else if (caller != c->gs) {
     if (hipEventRecord(c->ev_in, caller) != hipSuccess) return QE_ERR_HIP;
     if (hipStreamWaitEvent(c->gs, c->ev_in, 0) != hipSuccess) return QE_ERR_HIP;
   }
+  if (copy_all(pre, s) != hipSuccess) return QE_ERR_HIP;
+  hipEvent_t done = on_caller ? c->ev_chain : c->ev_tail;
   if (c->cfg.use_graphs) {
     GraphEntry &e = c->graphs[gkey];
-    if (e.exec == nullptr || !same_plan(e.plan, plan)) {
-      const auto t0 = std::chrono::steady_clock::now();
-      if (e.exec != nullptr) {
-        (void)hipGraphExecDestroy(e.exec);
-        e.exec = nullptr;
-      }
-      hipGraph_t graph = nullptr;
-      if (hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal) != hipSuccess) return QE_ERR_HIP;
-      hipError_t le = enqueue(c, plan, false, c->gs);
-      // The action's completion event is a node of the graph: recorded by the
-      // replay itself on the stream it runs on.  (On MI355X a separate record
-      // after the launch adds about 5 us of device time per action; the node
-      // adds none.)
-      if (le == hipSuccess) le = hipEventRecord(on_caller ? c->ev_chain : c->ev_tail, c->gs);
-      const hipError_t ce = hipStreamEndCapture(c->gs, &graph);
-      if (le != hipSuccess || ce != hipSuccess || graph == nullptr) {
-        if (graph) (void)hipGraphDestroy(graph);
-        return QE_ERR_HIP;
-      }
-      const hipError_t ie = hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(graph);
-      if (ie != hipSuccess) {
-        e.exec = nullptr;
-        return QE_ERR_HIP;
-      }
-      e.plan = plan;
-      c->st.captures += 1;
-      c->st.capture_ns +=
-          std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
-    }
+    const qe_status bs = bind_graph(c, e, plan);
+    if (bs != QE_OK) return bs;
     if (hipGraphLaunch(e.exec, s) != hipSuccess) return QE_ERR_HIP;
+    e.launched = true;
     c->st.replays += 1;
+    done = e.done;  // the graph's own event: a rebind waits for exactly this replay
   } else {
     if (enqueue(c, plan, c->timing != 0, s) != hipSuccess) return QE_ERR_HIP;
-    if (hipEventRecord(on_caller ? c->ev_chain : c->ev_tail, s) != hipSuccess) return QE_ERR_HIP;
   }
-  if (on_caller) {
-    c->has_last = true;
-    return QE_OK;
-  }
+  if (copy_all(post, s) != hipSuccess) return QE_ERR_HIP;
+  if (hipEventRecord(done, s) != hipSuccess) return QE_ERR_HIP;
+  c->last_ev = done;
+  c->has_last = true;
+  if (on_caller) return QE_OK;
   if (!c->cfg.one_way_handoff && caller != c->gs) {
-    if (hipStreamWaitEvent(caller, c->ev_tail, 0) != hipSuccess) return QE_ERR_HIP;
+    if (hipStreamWaitEvent(caller, done, 0) != hipSuccess) return QE_ERR_HIP;
   }
   c->st.handoffs += 2;
   return QE_OK;
@@ -415,6 +565,11 @@ void append_wgrad(Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, float 
   c.c.accumulate = mode == QE_PLACE_ACCUM;
   p.push_back(c);
 }
+
+size_t esize(int dt) { return dt == QE_BF16 ? 2 : 4; }
+
+// QE_GRAPH_INPUTS_COPY: graphs bind the layer's static buffers.
+bool copy_inputs(const qe_ctx *c) { return c->cfg.use_graphs && c->cfg.graph_inputs == QE_GRAPH_INPUTS_COPY; }
 
 qe_status fail_physical(qe_ctx *c) {
   c->contract.abort_epoch();
@@ -627,6 +782,8 @@ qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host) {
   // the one-way (testing) handoff only exists for the graph stream
   if (cfg_host->replay_on_caller != 0 && (cfg_host->replay_on_caller != 1 || cfg_host->one_way_handoff != 0))
     return QE_ERR_INVALID_ARG;
+  if (cfg_host->graph_inputs < QE_GRAPH_INPUTS_REBIND || cfg_host->graph_inputs > QE_GRAPH_INPUTS_COPY)
+    return QE_ERR_INVALID_ARG;
   *out_host = nullptr;
   qe_ctx *c = new (std::nothrow) qe_ctx(*cfg_host);
   if (c == nullptr) return QE_ERR_HIP;
@@ -667,8 +824,11 @@ void qe_ctx_destroy(qe_ctx *c) {
   if (!c->cfg.null_executor) {
     DeviceGuard dg(c->cfg.device);
     if (c->gs) (void)sync_actions(c);
-    for (auto &kv : c->graphs)
+    for (auto &kv : c->graphs) {
       if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
+      if (kv.second.graph) (void)hipGraphDestroy(kv.second.graph);
+      if (kv.second.done) (void)hipEventDestroy(kv.second.done);
+    }
     for (auto &L : c->layers)
       for (void *p : L.allocs) (void)hipFree(p);
     for (auto &t : c->timed) {
@@ -677,6 +837,7 @@ void qe_ctx_destroy(qe_ctx *c) {
     }
     for (hipEvent_t e : c->event_pool) (void)hipEventDestroy(e);
     if (c->d_token) (void)hipFree(c->d_token);
+    if (c->placeholder) (void)hipFree(c->placeholder);
     if (c->ev_in) (void)hipEventDestroy(c->ev_in);
     if (c->ev_tail) (void)hipEventDestroy(c->ev_tail);
     if (c->ev_chain) (void)hipEventDestroy(c->ev_chain);
@@ -720,6 +881,14 @@ qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_ou
     L.dy_q = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->max_tokens) * L.ld_dyq, &ok));
     if (c->cfg.copy_gradients)
       L.grad_stage = static_cast<float *>(dev_alloc(c, L, sizeof(float) * size_t(d->n_out) * size_t(d->k_in), &ok));
+    if (c->cfg.use_graphs && c->cfg.graph_inputs == QE_GRAPH_INPUTS_COPY) {
+      const size_t xb = sizeof(float) * size_t(d->max_tokens) * size_t(d->k_in);
+      const size_t yb = sizeof(float) * size_t(d->max_tokens) * size_t(d->n_out);
+      L.x_st = dev_alloc(c, L, xb, &ok);
+      L.dx_st = dev_alloc(c, L, xb, &ok);
+      L.y_st = dev_alloc(c, L, yb, &ok);
+      L.dy_st = dev_alloc(c, L, yb, &ok);
+    }
     for (auto &S : L.slots) {
       S.x_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->k_in) * L.ld_t, &ok));
       S.dy_q_t = static_cast<uint8_t *>(dev_alloc(c, L, size_t(d->n_out) * L.ld_t, &ok));
@@ -801,9 +970,18 @@ qe_status qe_fp8_linear_fwd(qe_ctx *c, int32_t layer, qe_tape_key key, const voi
   if (c->contract.physical_fails()) return fail_physical(c);
   if (!c->cfg.null_executor) {
     const LayerDev &L = c->layers[size_t(layer)];
-    const Plan p = plan_fwd(c, L, key.microbatch, x, x_dtype, tokens, y, y_dtype, refresh);
+    std::vector<Copy> pre, post;
+    const void *xg = x;
+    void *yg = y;
+    if (copy_inputs(c)) {
+      xg = L.x_st;
+      yg = L.y_st;
+      pre.push_back({L.x_st, x, size_t(tokens) * size_t(L.desc.k_in) * esize(x_dtype)});
+      post.push_back({y, L.y_st, size_t(tokens) * size_t(L.desc.n_out) * esize(y_dtype)});
+    }
+    const Plan p = plan_fwd(c, L, key.microbatch, xg, x_dtype, tokens, yg, y_dtype, refresh);
     if (run_plan(c, p, graph_key(layer, refresh ? ACT_FWD_REFRESH : ACT_FWD, key.microbatch),
-                 static_cast<hipStream_t>(caller)) != QE_OK)
+                 static_cast<hipStream_t>(caller), pre, post) != QE_OK)
       return fail_physical(c);
   }
   *ref_out_host = c->contract.commit_fwd(layer, key, tokens, refresh);
@@ -821,10 +999,20 @@ qe_status qe_fp8_linear_dgrad(qe_ctx *c, int32_t layer, qe_tape_key key, qe_tape
   if (c->contract.physical_fails()) return fail_physical(c);
   if (!c->cfg.null_executor) {
     const LayerDev &L = c->layers[size_t(layer)];
+    std::vector<Copy> pre, post;
+    const void *dyg = dy;
+    void *dxg = dx;
+    if (copy_inputs(c)) {
+      dyg = L.dy_st;
+      dxg = L.dx_st;
+      pre.push_back({L.dy_st, dy, size_t(tokens) * size_t(L.desc.n_out) * esize(dy_dtype)});
+      post.push_back({dx, L.dx_st, size_t(tokens) * size_t(L.desc.k_in) * esize(dx_dtype)});
+    }
     Plan p;
-    append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
+    append_dgrad(c, p, L, ref.slot, tokens, dyg, dy_dtype, dxg, dx_dtype);
     finish_dgrad(c, p, L);
-    if (run_plan(c, p, graph_key(layer, ACT_DGRAD, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
+    if (run_plan(c, p, graph_key(layer, ACT_DGRAD, ref.slot), static_cast<hipStream_t>(caller), pre, post) !=
+        QE_OK)
       return fail_physical(c);
   }
   c->contract.commit_dgrad(layer, ref);
@@ -863,11 +1051,20 @@ qe_status qe_fp8_linear_bwd_full(qe_ctx *c, int32_t layer, qe_tape_key key, qe_t
   if (c->contract.physical_fails()) return fail_physical(c);
   if (!c->cfg.null_executor) {
     const LayerDev &L = c->layers[size_t(layer)];
+    std::vector<Copy> pre, post;
+    const void *dyg = dy;
+    void *dxg = dx;
+    if (copy_inputs(c)) {
+      dyg = L.dy_st;
+      dxg = L.dx_st;
+      pre.push_back({L.dy_st, dy, size_t(tokens) * size_t(L.desc.n_out) * esize(dy_dtype)});
+      post.push_back({dx, L.dx_st, size_t(tokens) * size_t(L.desc.k_in) * esize(dx_dtype)});
+    }
     Plan p;
-    append_dgrad(c, p, L, ref.slot, tokens, dy, dy_dtype, dx, dx_dtype);
+    append_dgrad(c, p, L, ref.slot, tokens, dyg, dy_dtype, dxg, dx_dtype);
     append_wgrad(p, L, ref.slot, tokens, main_grad, offset, ld, mode);
     finish_dgrad(c, p, L);
-    if (run_plan(c, p, graph_key(layer, ACT_FULL, ref.slot), static_cast<hipStream_t>(caller)) != QE_OK)
+    if (run_plan(c, p, graph_key(layer, ACT_FULL, ref.slot), static_cast<hipStream_t>(caller), pre, post) != QE_OK)
       return fail_physical(c);
   }
   c->contract.commit_bwd_full(layer, ref);
@@ -879,6 +1076,71 @@ qe_status qe_arena_bind(qe_ctx *c, int32_t layer, uint32_t microbatch, float *bu
                         int64_t ld) {
   if (c == nullptr) return QE_ERR_INVALID_ARG;
   return c->contract.bind(layer, int64_t(microbatch), reinterpret_cast<uintptr_t>(buf), buf_elems, offset, ld);
+}
+
+qe_status qe_prebuild_graphs(qe_ctx *c, const qe_prebuild_desc *d) {
+  if (c == nullptr || d == nullptr || d->tokens < 0 || !valid_dtype(d->x_dtype) || !valid_dtype(d->y_dtype) ||
+      !valid_dtype(d->dy_dtype) || !valid_dtype(d->dx_dtype))
+    return QE_ERR_INVALID_ARG;
+  if (!c->cfg.use_graphs) return QE_ERR_INVALID_ARG;
+  for (const auto &L : c->layers)
+    if (d->tokens > L.desc.max_tokens) return QE_ERR_INVALID_ARG;
+  if (c->cfg.null_executor) return QE_OK;
+  DeviceGuard dg(c->cfg.device);
+  if (!dg.ok) return QE_ERR_HIP;
+  const auto t0 = std::chrono::steady_clock::now();
+  const bool cp = copy_inputs(c);
+  const int M = c->cfg.microbatches;
+  if (!cp && c->placeholder == nullptr) {
+    size_t bytes = 16;
+    for (const auto &L : c->layers) {  // max_tokens rows: enough for any later prebuild too
+      const size_t t = size_t(L.desc.max_tokens);
+      const size_t w = size_t(L.desc.k_in > L.desc.n_out ? L.desc.k_in : L.desc.n_out);
+      bytes = t * w * sizeof(float) > bytes ? t * w * sizeof(float) : bytes;
+    }
+    if (hipMalloc(&c->placeholder, bytes) != hipSuccess) {
+      c->placeholder = nullptr;
+      return QE_ERR_HIP;
+    }
+    c->st.device_bytes += int64_t(bytes);
+  }
+  for (int l = 0; l < int(c->layers.size()); ++l) {
+    const LayerDev &L = c->layers[size_t(l)];
+    const qe::LayerBook &B = c->contract.layer(l);
+    const int64_t t = d->tokens > 0 ? d->tokens : L.desc.max_tokens;
+    // Dynamic buffers are unknown here: the graphs bind the placeholder in
+    // their place until the first call binds its own.
+    const void *xg = cp ? L.x_st : c->placeholder;
+    void *yg = cp ? L.y_st : c->placeholder;
+    const void *dyg = cp ? L.dy_st : c->placeholder;
+    void *dxg = cp ? L.dx_st : c->placeholder;
+    for (int m = 0; m < M; ++m) {
+      // F (microbatch 0 refreshes the weight cache: it is the first forward
+      // after every optimizer commit), dI, and dW into the bound view
+      const bool refresh = m == 0;
+      const Plan pf = plan_fwd(c, L, uint32_t(m), xg, d->x_dtype, t, yg, d->y_dtype, refresh);
+      qe_status st = bind_graph(c, c->graphs[graph_key(l, refresh ? ACT_FWD_REFRESH : ACT_FWD, uint32_t(m))], pf);
+      if (st != QE_OK) return st;
+      Plan pd;
+      append_dgrad(c, pd, L, uint32_t(m), t, dyg, d->dy_dtype, dxg, d->dx_dtype);
+      finish_dgrad(c, pd, L);
+      st = bind_graph(c, c->graphs[graph_key(l, ACT_DGRAD, uint32_t(m))], pd);
+      if (st != QE_OK) return st;
+      const qe::View &V = B.views[size_t(m)];
+      if (!V.bound) continue;
+      // a microbatch whose view an earlier microbatch shares accumulates
+      int mode = QE_PLACE_INIT;
+      for (int m2 = 0; m2 < m; ++m2)
+        if (B.views[size_t(m2)].bound && B.views[size_t(m2)].start() == V.start()) mode = QE_PLACE_ACCUM;
+      Plan pw;
+      append_wgrad(pw, L, uint32_t(m), t, reinterpret_cast<float *>(V.buf), V.offset, V.ld, mode);
+      st = bind_graph(c, c->graphs[graph_key(l, ACT_WGRAD, uint32_t(m))], pw);
+      if (st != QE_OK) return st;
+    }
+  }
+  c->st.prebuild_ns +=
+      std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
+  return QE_OK;
 }
 
 qe_status qe_arena_finalize(qe_ctx *c) { return c ? c->contract.finalize() : QE_ERR_INVALID_ARG; }

@@ -701,11 +701,10 @@ hipError_t launch_w4(const GemmParams &g, hipStream_t s) {
   const int vec_ok = (g.out == 1) ? (g.ldc % 4 == 0 && cp % 8 == 0) : (g.ldc % 4 == 0 && cp % 16 == 0);
   const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n)), block(256);
   switch (g.out) {
-    case 0: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 0, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    case 1: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 1, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    default: hipLaunchKernelGGL((gemm_tn_w4_kernel<FA, FB, 2, BM, BN>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    case 0: return klaunch(gemm_tn_w4_kernel<FA, FB, 0, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
+    case 1: return klaunch(gemm_tn_w4_kernel<FA, FB, 1, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
+    default: return klaunch(gemm_tn_w4_kernel<FA, FB, 2, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
   }
-  return hipGetLastError();
 }
 
 template <int BM, int BN>
@@ -723,11 +722,10 @@ hipError_t launch_out(const GemmParams &g, hipStream_t s) {
   const int vec_ok = (g.out == 1) ? (g.ldc % 4 == 0 && cp % 8 == 0) : (g.ldc % 4 == 0 && cp % 16 == 0);
   const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n)), block(WM * WN * 64);
   switch (g.out) {
-    case 0: hipLaunchKernelGGL((gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 0>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    case 1: hipLaunchKernelGGL((gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 1>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
-    default: hipLaunchKernelGGL((gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 2>), grid, block, 0, s, g, tiles_m, tiles_n, vec_ok); break;
+    case 0: return klaunch(gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 0>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
+    case 1: return klaunch(gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 1>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
+    default: return klaunch(gemm_tn_kernel<BM, BN, WM, WN, FA, FB, 2>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
   }
-  return hipGetLastError();
 }
 
 template <int BM, int BN, int WM, int WN>

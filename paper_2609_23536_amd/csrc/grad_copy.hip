@@ -59,14 +59,11 @@ hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s) {
   const bool vec = (p.k % 4 == 0) && (p.ld % 4 == 0) && (reinterpret_cast<uintptr_t>(p.src) % 16 == 0) &&
                    (reinterpret_cast<uintptr_t>(p.dst) % 16 == 0);
   const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
-  if (p.accumulate) {
-    if (vec) hipLaunchKernelGGL((grad_copy_kernel<true, true>), grid, block, 0, s, p, col_blocks);
-    else hipLaunchKernelGGL((grad_copy_kernel<true, false>), grid, block, 0, s, p, col_blocks);
-  } else {
-    if (vec) hipLaunchKernelGGL((grad_copy_kernel<false, true>), grid, block, 0, s, p, col_blocks);
-    else hipLaunchKernelGGL((grad_copy_kernel<false, false>), grid, block, 0, s, p, col_blocks);
-  }
-  return hipGetLastError();
+  if (p.accumulate)
+    return vec ? klaunch(grad_copy_kernel<true, true>, grid, block, 0, s, p, col_blocks)
+               : klaunch(grad_copy_kernel<true, false>, grid, block, 0, s, p, col_blocks);
+  return vec ? klaunch(grad_copy_kernel<false, true>, grid, block, 0, s, p, col_blocks)
+             : klaunch(grad_copy_kernel<false, false>, grid, block, 0, s, p, col_blocks);
 }
 
 }  // namespace qe

@@ -3,8 +3,71 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <string.h>
+
+#include <vector>
 
 namespace qe {
+
+// One kernel launch: function, launch shape and argument bytes.  The launch
+// functions below go through klaunch(), which either launches the kernel on a
+// stream or, while a recording list is installed on the calling thread,
+// appends the launch to it without touching the device.  The executor records
+// an action's launches to compare them with the kernel nodes of the graph it
+// captured earlier and to rewrite the arguments of those nodes in place when
+// only the arguments differ (hipGraphExecKernelNodeSetParams).
+constexpr int kMaxKernelArgs = 8;
+constexpr int kKernelArgBytes = 1024;
+struct KernelRec {
+  const void *func;
+  dim3 grid, block;
+  uint32_t shmem;
+  uint32_t nargs;
+  uint32_t used;  // bytes of blob in use
+  uint16_t off[kMaxKernelArgs];
+  alignas(16) uint8_t blob[kKernelArgBytes];
+  KernelRec() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
+  // argument pointers for hipLaunchKernel / kernel-node parameters
+  void argv(void **out) const {
+    for (uint32_t i = 0; i < nargs; ++i) out[i] = const_cast<uint8_t *>(blob) + off[i];
+  }
+  bool same_shape(const KernelRec &o) const {
+    return func == o.func && grid.x == o.grid.x && grid.y == o.grid.y && grid.z == o.grid.z &&
+           block.x == o.block.x && block.y == o.block.y && block.z == o.block.z && shmem == o.shmem &&
+           nargs == o.nargs && used == o.used && memcmp(off, o.off, sizeof(off)) == 0;
+  }
+  bool same_args(const KernelRec &o) const { return memcmp(blob, o.blob, used) == 0; }
+};
+
+// Installed by the executor on the calling thread while it records a plan.
+extern thread_local std::vector<KernelRec> *tl_record;
+
+template <typename T>
+inline void pack_arg(KernelRec &r, const T &v) {
+  static_assert(sizeof(T) <= 512, "kernel argument too large");
+  uint32_t o = (r.used + uint32_t(alignof(T)) - 1) & ~(uint32_t(alignof(T)) - 1);
+  memcpy(r.blob + o, &v, sizeof(T));
+  r.off[r.nargs++] = uint16_t(o);
+  r.used = o + uint32_t(sizeof(T));
+}
+
+template <typename... P, typename... A>
+hipError_t klaunch(void (*f)(P...), dim3 grid, dim3 block, size_t shmem, hipStream_t s, const A &...a) {
+  static_assert(sizeof...(P) == sizeof...(A) && sizeof...(P) <= kMaxKernelArgs, "kernel arguments");
+  KernelRec r;
+  r.func = reinterpret_cast<const void *>(f);
+  r.grid = grid;
+  r.block = block;
+  r.shmem = uint32_t(shmem);
+  (pack_arg<P>(r, P(a)), ...);
+  if (tl_record != nullptr) {
+    tl_record->push_back(r);
+    return hipSuccess;
+  }
+  void *argv[kMaxKernelArgs];
+  r.argv(argv);
+  return hipLaunchKernel(r.func, grid, block, argv, shmem, s);
+}
 
 constexpr int kMaxMetas = 8;
 constexpr int kMaxHistory = 8192;

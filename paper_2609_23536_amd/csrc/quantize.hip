@@ -254,15 +254,13 @@ template <bool BF16>
 hipError_t launch_fmt(const QuantPair &pp, int fmt, hipStream_t s) {
   int64_t tiles = 0;
   for (int i = 0; i < pp.n; ++i) tiles += pp.j[i].tiles;
-  if (fmt == 0)
-    hipLaunchKernelGGL((quantize_kernel<BF16, 0>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
-  else
-    hipLaunchKernelGGL((quantize_kernel<BF16, 1>), dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
-  return hipGetLastError();
+  if (fmt == 0) return klaunch(quantize_kernel<BF16, 0>, dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
+  return klaunch(quantize_kernel<BF16, 1>, dim3(unsigned(tiles)), dim3(kThreads), 0, s, pp);
 }
 
 QuantJob make_job(const QuantParams &p) {
-  QuantJob j{};
+  QuantJob j;
+  memset(&j, 0, sizeof(j));  // padding too: recorded launches are compared bytewise
   j.p = p;
   const int64_t tiles_r = (p.rows + kTile - 1) / kTile;
   const int64_t tiles_c = (p.cols + kTile - 1) / kTile;
@@ -284,7 +282,8 @@ hipError_t launch_pair(const QuantPair &pp, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s) {
-  QuantPair pp{};
+  QuantPair pp;
+  memset(&pp, 0, sizeof(pp));
   pp.j[0] = make_job(p);
   pp.n = 1;
   return launch_pair(pp, s);
@@ -295,7 +294,8 @@ hipError_t launch_quantize_pair(const QuantParams &a, const QuantParams &b, hipS
     const hipError_t e = launch_quantize(a, s);
     return e != hipSuccess ? e : launch_quantize(b, s);
   }
-  QuantPair pp{};
+  QuantPair pp;
+  memset(&pp, 0, sizeof(pp));
   pp.j[0] = make_job(a);
   pp.j[1] = make_job(b);
   pp.n = 2;

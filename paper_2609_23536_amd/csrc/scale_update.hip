@@ -109,8 +109,7 @@ hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s) {
   int hmax = 0;
   for (int i = 0; i < p.n; ++i) hmax = p.m[i].history_len > hmax ? p.m[i].history_len : hmax;
   size_t lds = size_t(hmax) * sizeof(uint32_t);
-  hipLaunchKernelGGL(scale_update_kernel, dim3(p.n), dim3(kThreads), lds, s, p);
-  return hipGetLastError();
+  return klaunch(scale_update_kernel, dim3(p.n), dim3(kThreads), lds, s, p);
 }
 
 }  // namespace qe

@@ -22,6 +22,7 @@ ROLE_X, ROLE_W, ROLE_DY = 0, 1, 2
 SCALING_DELAYED, SCALING_CURRENT = 0, 1
 AMAX_LINES, AMAX_STRIDE = 64, 64   # amax accumulator: lines x floats between lines
 KC_QUANT, KC_UPDATE, KC_GEMM, KC_COPY, KC_AMAX = 0, 1, 2, 3, 4
+GRAPH_INPUTS_REBIND, GRAPH_INPUTS_RECAPTURE, GRAPH_INPUTS_COPY = 0, 1, 2
 
 STATUS = ["OK", "INVALID_ARG", "STALE_REF", "KEY_MISMATCH", "KEY_LIVE", "POOL_FULL", "DUPLICATE_CONSUMER", "ORDER",
           "EPOCH", "STALE_CACHE", "DEST_MISMATCH", "DEST_ALIAS", "DUP_WRITE", "ARENA_INVALID", "INCOMPLETE",
@@ -52,7 +53,7 @@ class FP8Meta(C.Structure):
 class Config(C.Structure):
     _fields_ = [("device", C.c_int32), ("microbatches", C.c_int32), ("use_graphs", C.c_int32),
                 ("null_executor", C.c_int32), ("one_way_handoff", C.c_int32), ("copy_gradients", C.c_int32),
-                ("replay_on_caller", C.c_int32), ("reserved", C.c_int32)]
+                ("replay_on_caller", C.c_int32), ("graph_inputs", C.c_int32)]
 
 
 class LayerDesc(C.Structure):
@@ -66,7 +67,13 @@ class CtxState(C.Structure):
     _fields_ = [("e_w", C.c_int64), ("token", C.c_int64), ("device_token", C.c_int64), ("arena_valid", C.c_int32),
                 ("finalized", C.c_int32), ("graphs", C.c_int64), ("captures", C.c_int64), ("replays", C.c_int64),
                 ("handoffs", C.c_int64), ("capture_ns", C.c_int64), ("arena_bytes", C.c_int64),
-                ("device_bytes", C.c_int64)]
+                ("device_bytes", C.c_int64), ("rebinds", C.c_int64), ("rebound_nodes", C.c_int64),
+                ("prebuild_ns", C.c_int64)]
+
+
+class PrebuildDesc(C.Structure):
+    _fields_ = [("tokens", C.c_int64), ("x_dtype", C.c_int32), ("y_dtype", C.c_int32), ("dy_dtype", C.c_int32),
+                ("dx_dtype", C.c_int32)]
 
 
 class LayerState(C.Structure):
@@ -98,6 +105,7 @@ _SIGS = {
     "qe_fp8_linear_wgrad_place": [_P, _I32, TapeKey, TapeRef, _P, _I64, _I64, _I32, _P],
     "qe_fp8_linear_bwd_full": [_P, _I32, TapeKey, TapeRef, _P, _I32, _P, _I32, _P, _I64, _I64, _I32, _P],
     "qe_arena_bind": [_P, _I32, _U32, _P, _I64, _I64, _I64],
+    "qe_prebuild_graphs": [_P, C.POINTER(PrebuildDesc)],
     "qe_arena_finalize": [_P],
     "qe_optimizer_commit": [_P],
     "qe_abort_epoch": [_P],
@@ -213,9 +221,10 @@ class Context:
     """Owns one qe_ctx.  Methods forward to the C calls of the same name."""
 
     def __init__(self, microbatches: int, use_graphs: bool = False, null_executor: bool = False, device: int = 0,
-                 one_way_handoff: bool = False, copy_gradients: bool = False, replay_on_caller: bool = False):
+                 one_way_handoff: bool = False, copy_gradients: bool = False, replay_on_caller: bool = False,
+                 graph_inputs: int = GRAPH_INPUTS_REBIND):
         cfg = Config(device, microbatches, int(use_graphs), int(null_executor), int(one_way_handoff),
-                     int(copy_gradients), int(replay_on_caller))
+                     int(copy_gradients), int(replay_on_caller), int(graph_inputs))
         h = C.c_void_p()
         st = _st(lib().qe_ctx_create(C.byref(cfg), C.byref(h)))
         if st != "OK":
@@ -287,6 +296,10 @@ class Context:
 
     def qe_arena_bind(self, layer: int, microbatch: int, buf, buf_elems: int, offset: int, ld: int) -> str:
         return _st(lib().qe_arena_bind(self.h, layer, microbatch, ptr(buf), buf_elems, offset, ld))
+
+    def qe_prebuild_graphs(self, tokens: int, x_dtype: int, y_dtype: int, dy_dtype: int, dx_dtype: int) -> str:
+        d = PrebuildDesc(tokens, x_dtype, y_dtype, dy_dtype, dx_dtype)
+        return _st(lib().qe_prebuild_graphs(self.h, C.byref(d)))
 
     def qe_arena_finalize(self) -> str:
         return _st(lib().qe_arena_finalize(self.h))

@@ -1,7 +1,11 @@
 """Caller / graph stream handoff (§2.3 and Table "correctness", stream-ordering
 row): with the two-way handoff a consumer enqueued on the caller stream right
 after a replayed action always sees the action's final output; with only the
-one-way edge (testing mode) it can observe stale data."""
+one-way edge (testing mode) it can observe stale data.  Checked with an
+explicit caller stream and with the default stream, graph replay and direct
+launches: a completion event recorded by a node inside the graph was found
+not to order a waiting stream on this runtime, so the executor records it
+after the launch, and these trials are what shows that it orders."""
 import pytest
 
 from tests.gpu_util import dev, torch
@@ -10,11 +14,11 @@ from tests.libqe import need_lib
 pytestmark = pytest.mark.gpu
 
 
-def stale_count(one_way: bool, trials: int) -> int:
+def stale_count(one_way: bool, trials: int, default_stream: bool = False, use_graphs: bool = True) -> int:
     qe = need_lib()
     d = dev()
     n, k, t = 28672, 4096, 4096
-    ctx = qe.Context(1, use_graphs=True, one_way_handoff=one_way)
+    ctx = qe.Context(1, use_graphs=use_graphs, one_way_handoff=one_way)
     g = torch.Generator(device=d)
     g.manual_seed(1)
     w = (torch.randn(n, k, device=d, generator=g) * 0.02).to(torch.bfloat16)
@@ -22,7 +26,7 @@ def stale_count(one_way: bool, trials: int) -> int:
     st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.BF16, 4, 0)
     assert st == "OK"
     y = torch.empty((t, n), dtype=torch.bfloat16, device=d)
-    caller = torch.cuda.Stream()
+    caller = torch.cuda.default_stream(d) if default_stream else torch.cuda.Stream()
     stale = 0
     for trial in range(trials):
         with torch.cuda.stream(caller):
@@ -40,8 +44,10 @@ def stale_count(one_way: bool, trials: int) -> int:
     return stale
 
 
-def test_two_way_handoff_never_stale():
-    assert stale_count(one_way=False, trials=30) == 0
+@pytest.mark.parametrize("default_stream", [False, True], ids=["explicit_stream", "default_stream"])
+@pytest.mark.parametrize("use_graphs", [True, False], ids=["graphs", "eager"])
+def test_two_way_handoff_never_stale(default_stream, use_graphs):
+    assert stale_count(one_way=False, trials=30, default_stream=default_stream, use_graphs=use_graphs) == 0
 
 
 def test_one_way_handoff_is_observably_stale():

@@ -349,3 +349,29 @@ def _fnv1a(b):
     for x in b:
         h = ((h ^ x) * 1099511628211) % (1 << 64)
     return h
+
+
+def test_prebuild_graphs_argument_checks():
+    """qe_prebuild_graphs validates before doing anything (host-only context)."""
+    from tests.libqe import need_lib
+    qe = need_lib()
+    nog = qe.Context(2, use_graphs=False, null_executor=True)
+    assert nog.qe_prebuild_graphs(0, qe.BF16, qe.F32, qe.BF16, qe.F32) == "INVALID_ARG"
+    nog.close()
+    c = qe.Context(2, use_graphs=True, null_executor=True)
+    st, idx = c.qe_layer_register(0, 0, 64, 32, 100, None, qe.F32, 4, 0)
+    assert st == "OK"
+    assert c.qe_prebuild_graphs(101, qe.BF16, qe.F32, qe.BF16, qe.F32) == "INVALID_ARG"
+    assert c.qe_prebuild_graphs(-1, qe.BF16, qe.F32, qe.BF16, qe.F32) == "INVALID_ARG"
+    assert c.qe_prebuild_graphs(0, 7, qe.F32, qe.BF16, qe.F32) == "INVALID_ARG"
+    assert c.qe_prebuild_graphs(100, qe.BF16, qe.F32, qe.BF16, qe.F32) == "OK"
+    assert c.qe_get_state()["captures"] == 0  # no device: nothing captured
+    c.close()
+
+
+def test_graph_inputs_mode_checked():
+    from tests.libqe import need_lib
+    qe = need_lib()
+    for bad in (-1, 3):
+        with pytest.raises(RuntimeError):
+            qe.Context(1, use_graphs=True, null_executor=True, graph_inputs=bad)

@@ -32,7 +32,8 @@ def test_struct_sizes():
     qe = need_lib()
     pairs = {"qe_tape_key": qe.TapeKey, "qe_tape_ref": qe.TapeRef, "qe_fp8_meta": qe.FP8Meta,
              "qe_config": qe.Config, "qe_layer_desc": qe.LayerDesc, "qe_ctx_state": qe.CtxState,
-             "qe_layer_state": qe.LayerState, "qe_slot_state": qe.SlotState}
+             "qe_layer_state": qe.LayerState, "qe_slot_state": qe.SlotState,
+             "qe_prebuild_desc": qe.PrebuildDesc}
     if shutil.which("gcc") is None:
         pytest.skip("no C compiler")
     inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
