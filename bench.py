@@ -3,36 +3,46 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--eager]
 
 A step runs, for every linear of the stage (QKV, O, gate+up, down of the
-Llama-3-8B shape by default, 4096 tokens, bf16 inputs and master weights,
-amax history 1024):  F (with the weight-cache refresh, since every step
-follows a version bump), then dI and the deferred dW with direct placement
-into one flat FP32 main-gradient buffer, then arena finalize and optimizer
-commit.  Every action is one HIP-graph replay, by default on the caller's
-stream (stream order gives both directions of the handoff; --executor two-way
-runs the paper's two-way handoff through the library's graph stream instead,
-and the line reports the other executor's step time beside the headline).
-Inputs are synthetic, seeded, and resident in HBM before timing starts.
+Llama-3-70B shape by default, one microbatch of 8192 tokens, bf16 inputs and
+master weights, amax history 1024):  F (with the weight-cache refresh, since
+every step follows a version bump), then dI and the deferred dW with direct
+placement into one flat FP32 main-gradient buffer, then arena finalize and
+optimizer commit.  The stage's graphs are captured before the first step
+(qe_prebuild_graphs) and every action is one HIP-graph replay, by default on
+the caller's stream (stream order gives both directions of the handoff;
+--executor two-way runs the paper's two-way handoff through the library's
+graph stream instead, and the line reports the other executor's step time
+beside the headline).  Inputs are synthetic, seeded, and resident in HBM
+before timing starts.
 
 Prints one JSON line.  `value` is GEMM FLOPs (fwd + dI + dW, 2*M*N*K each)
 per second over the whole step, quantization and scale updates included.
 `roofline` is the GEMM kernel alone, timed with HIP events on the stream the
 library launches it on, in an instrumented eager pass over the same steps.
-`cpu_baseline` times the CPU oracle on a bounded sample (the stage's linears
-in order, at full token count, until at least 10 s of CPU work).  Beside the
-headline the line carries the same steps under the other executor, with the
-actions' kernels launched the other way (direct launches against graph
-replay), with copied gradients, with current scaling and after a checkpoint
-restart; per-action latencies of a single small linear; and the deferred dW
-GEMM alone at the zero-bubble microbatch, INIT- and ACCUM-placed.  One
-progress line per finished pass goes to stderr.
+`cpu_baseline` times the CPU oracle stage by stage on a bounded sample of the
+same workload.  Beside the headline the line carries the same steps under the
+other executor, with the actions' kernels launched the other way (direct
+launches against graph replay), with copied gradients, with current scaling,
+after a checkpoint restart, and with the caller's buffers rotated every step
+under the three ways a replayed graph meets new buffers; per-action latencies
+of a single small linear; and the deferred dW GEMM alone at the zero-bubble
+microbatch, INIT- and ACCUM-placed.  A progress line after every setup phase
+and every pass goes to stderr.
 """
 from __future__ import annotations
 
-import argparse
-import json
 import os
-import sys
-import time
+
+# Thread counts of the CPU oracle's BLAS, fixed before NumPy loads (a value
+# already in the environment wins).
+_THREADS = os.environ.get("OMP_NUM_THREADS") or str(min(16, len(os.sched_getaffinity(0))))
+os.environ.setdefault("OMP_NUM_THREADS", _THREADS)
+os.environ.setdefault("OPENBLAS_NUM_THREADS", _THREADS)
+
+import argparse  # noqa: E402
+import json  # noqa: E402
+import sys  # noqa: E402
+import time  # noqa: E402
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -47,7 +57,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama3_8b_stage_4096tok")
+    ap.add_argument("--workload", default="llama3_70b_stage_8192tok")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true",
@@ -65,25 +75,26 @@ def parse():
                     help="skip the dW-placement measurement at the zero-bubble workload's 2048-token microbatch")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-action latency of the small single-linear schedule")
-    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--no-rotate", action="store_true",
+                    help="skip the passes with the caller's buffers rotated every step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama3_8b_stage_4096tok_traffic.txt")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_23536_amd", "csrc", "gemm_fp8.hip")
 
 
 def gemm_traffic_per_launch(workload):
-    """HBM bytes per GEMM launch from the committed counter runs, or None when
-    they were taken on another workload or a different GEMM kernel source than
-    the current one."""
+    """HBM bytes per GEMM launch from the committed counter runs on this
+    workload, or None when there are none or they were taken on a different
+    GEMM kernel source than the current one."""
     import hashlib
-    if not os.path.exists(TRAFFIC_FILE):
+    path = os.path.join(ROOT, "profiles", f"gemm_{workload}_traffic.txt")
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
@@ -106,40 +117,60 @@ def copy_calibration(nbytes):
 _RESIDENT = {}  # workload -> (weights, inputs, output gradients) on the device
 
 
+def resident_inputs(torch, wl, device):
+    """The seeded weights, inputs and output gradients of `wl`, generated on the
+    host once per workload and kept on the device (every pass only reads them)."""
+    import numpy as np
+    import workloads as W
+    key = (wl.key, str(device))
+    if key in _RESIDENT:
+        return _RESIDENT[key]
+    _RESIDENT.clear()
+    bf = wl.in_dtype == "bf16"
+
+    def up(t):
+        a = t.data.view(np.int16) if bf else t.data
+        return torch.from_numpy(a).to(device)
+
+    ws, xs, dys = [], [], []
+    for u, lin in enumerate(wl.linears):
+        t0 = time.perf_counter()
+        ws.append(up(W.layer_weight(wl, u)))
+        inp = W.layer_inputs(wl, u)
+        xs.append(up(inp["x"]))
+        dys.append(up(inp["dy"]))
+        del inp
+        progress(f"inputs of {lin.name} ({lin.k_in}->{lin.n_out}, {wl.tokens} tokens) generated and uploaded "
+                 f"in {time.perf_counter() - t0:.1f} s")
+    _RESIDENT[key] = (ws, xs, dys)
+    return _RESIDENT[key]
+
+
 class StageBench:
+    """One stage context over the workload's linears.  `rotate` > 1 hands every
+    action one of `rotate` sets of X / dY / Y / dX buffers in turn (as a
+    training loop hands the layer new activation and gradient tensors);
+    `prebuild` captures the stage's graphs before the first step."""
+
     def __init__(self, qe, torch, wl, use_graphs, device, copy_gradients=False, current=False,
-                 replay_on_caller=False):
-        import workloads as W
+                 replay_on_caller=False, graph_inputs=0, rotate=1, prebuild=True):
         self.qe, self.torch, self.wl, self.d = qe, torch, wl, device
         self.ctx = qe.Context(1, use_graphs=use_graphs, copy_gradients=copy_gradients,
-                              replay_on_caller=replay_on_caller)
+                              replay_on_caller=replay_on_caller, graph_inputs=graph_inputs)
         self.n_lin = len(wl.linears)
         bf = wl.in_dtype == "bf16"
         self.dt = qe.BF16 if bf else qe.F32
         tdt = torch.int16 if bf else torch.float32
-
-        def up(t):
-            import numpy as np
-            a = t.data.view(np.int16) if bf else t.data
-            return torch.from_numpy(a).to(device)
-
-        # the seeded weights and inputs are generated on the host once per
-        # workload and shared by every pass (the library only reads them)
-        key = (wl.key, str(device))
-        if key not in _RESIDENT:
-            ws, xs, dys = [], [], []
-            for u in range(len(wl.linears)):
-                ws.append(up(W.layer_weight(wl, u)))
-                inp = W.layer_inputs(wl, u)
-                xs.append(up(inp["x"]))
-                dys.append(up(inp["dy"]))
-            _RESIDENT.clear()
-            _RESIDENT[key] = (ws, xs, dys)
-        ws, xs, dys = _RESIDENT[key]
-        self.w, self.x, self.dy, self.y, self.dx = list(ws), list(xs), list(dys), [], []
+        ws, xs, dys = resident_inputs(torch, wl, device)
+        self.w = list(ws)
+        self.rotate = rotate
+        self.x = [[x] + [x.clone() for _ in range(rotate - 1)] for x in xs]
+        self.dy = [[dy] + [dy.clone() for _ in range(rotate - 1)] for dy in dys]
+        self.y = [[torch.empty((wl.tokens, lin.n_out), dtype=tdt, device=device) for _ in range(rotate)]
+                  for lin in wl.linears]
+        self.dx = [[torch.empty((wl.tokens, lin.k_in), dtype=tdt, device=device) for _ in range(rotate)]
+                   for lin in wl.linears]
         for u, lin in enumerate(wl.linears):
-            self.y.append(torch.empty((wl.tokens, lin.n_out), dtype=tdt, device=device))
-            self.dx.append(torch.empty((wl.tokens, lin.k_in), dtype=tdt, device=device))
             st, idx = self.ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, wl.tokens, self.w[u], self.dt,
                                                  1 if current else wl.history, wl.margin,
                                                  scaling=qe.SCALING_CURRENT if current else qe.SCALING_DELAYED)
@@ -149,25 +180,33 @@ class StageBench:
         for u, lin in enumerate(wl.linears):
             st = self.ctx.qe_arena_bind(u, 0, self.grad, self.grad.numel(), self.offs[u], lin.k_in)
             assert st == "OK", st
+        self.prebuild_ms = None
+        if use_graphs and prebuild:
+            st = self.ctx.qe_prebuild_graphs(wl.tokens, self.dt, self.dt, self.dt, self.dt)
+            assert st == "OK", st
+            self.prebuild_ms = self.ctx.qe_get_state()["prebuild_ns"] / 1e6
         self.epoch = 0
+        self.nstep = 0
 
     def step(self):
         qe, wl, ctx = self.qe, self.wl, self.ctx
+        r = self.nstep % self.rotate
         refs = []
         for u in range(self.n_lin):
-            st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(self.epoch, 0, 0, u), self.x[u], self.dt, wl.tokens,
-                                            self.y[u], self.dt)
+            st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(self.epoch, 0, 0, u), self.x[u][r], self.dt, wl.tokens,
+                                            self.y[u][r], self.dt)
             assert st == "OK", st
             refs.append(ref)
         for u in reversed(range(self.n_lin)):
             k = qe.key(self.epoch, 0, 0, u)
-            st = ctx.qe_fp8_linear_dgrad(u, k, refs[u], self.dy[u], self.dt, self.dx[u], self.dt)
+            st = ctx.qe_fp8_linear_dgrad(u, k, refs[u], self.dy[u][r], self.dt, self.dx[u][r], self.dt)
             assert st == "OK", st
             st = ctx.qe_fp8_linear_wgrad_place(u, k, refs[u], self.grad, self.offs[u], wl.linears[u].k_in, qe.INIT)
             assert st == "OK", st
         assert ctx.qe_arena_finalize() == "OK"
         assert ctx.qe_optimizer_commit() == "OK"
         self.epoch += 1
+        self.nstep += 1
 
 
 def per_action_latency(qe, torch, device, steps=200, warmup=10):
@@ -175,38 +214,56 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
     tokens, fp32 inputs, history 4, schedule F0 F1 dI0 dI1 dW0 dW1 (both dW into
     one shared view: INIT, then ACCUM), then finalize and commit.  Mean wall time
     per action: graph replay and direct launches, each behind the two-way
-    handoff (the graph stream) and on the caller's stream."""
+    handoff (the graph stream) and on the caller's stream; and, on the caller's
+    stream, with the caller's X / dY / Y / dX buffers rotated over three sets
+    every step under the three ways a replayed graph can meet new buffers
+    (kernel-node arguments rewritten in place, the paper's static buffers with
+    copies, a new capture)."""
     import numpy as np
     import workloads as W
     wl = W.WORKLOADS["single_linear_128x256x256"]
     lin = wl.linears[0]
+    R = 3
 
     def up(t):
         return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
 
-    res = {}
-    for mode in ("graph", "eager", "graph_on_caller", "eager_on_caller"):
-        ctx = qe.Context(wl.microbatches, use_graphs=mode.startswith("graph"), replay_on_caller=mode.endswith("caller"))
+    modes = {"graph": (True, False, qe.GRAPH_INPUTS_REBIND, 1), "eager": (False, False, 0, 1),
+             "graph_on_caller": (True, True, qe.GRAPH_INPUTS_REBIND, 1), "eager_on_caller": (False, True, 0, 1),
+             "rotate_rebind": (True, True, qe.GRAPH_INPUTS_REBIND, R),
+             "rotate_copy": (True, True, qe.GRAPH_INPUTS_COPY, R),
+             "rotate_recapture": (True, True, qe.GRAPH_INPUTS_RECAPTURE, R),
+             "rotate_eager": (False, True, 0, R)}
+    res, counters = {}, {}
+    for mode, (graphs, on_caller, gi, rot) in modes.items():
+        ctx = qe.Context(wl.microbatches, use_graphs=graphs, replay_on_caller=on_caller, graph_inputs=gi)
         w = up(W.layer_weight(wl, 0))
         st, idx = ctx.qe_layer_register(0, 0, lin.n_out, lin.k_in, wl.tokens, w, qe.F32, wl.history, wl.margin)
         assert st == "OK" and idx == 0, st
         grad = torch.zeros(lin.n_out * lin.k_in, dtype=torch.float32, device=device)
         for m in range(wl.microbatches):
             assert ctx.qe_arena_bind(0, m, grad, grad.numel(), 0, lin.k_in) == "OK"
-        xs = [up(W.layer_inputs(wl, 0, mb=m)["x"]) for m in range(wl.microbatches)]
-        dys = [up(W.layer_inputs(wl, 0, mb=m)["dy"]) for m in range(wl.microbatches)]
-        ys = [torch.empty((wl.tokens, lin.n_out), dtype=torch.float32, device=device) for _ in xs]
-        dxs = [torch.empty((wl.tokens, lin.k_in), dtype=torch.float32, device=device) for _ in xs]
+        if graphs:
+            assert ctx.qe_prebuild_graphs(wl.tokens, qe.F32, qe.F32, qe.F32, qe.F32) == "OK"
+        xs = [[up(W.layer_inputs(wl, 0, mb=m)["x"]) for _ in range(rot)] for m in range(wl.microbatches)]
+        dys = [[up(W.layer_inputs(wl, 0, mb=m)["dy"]) for _ in range(rot)] for m in range(wl.microbatches)]
+        ys = [[torch.empty((wl.tokens, lin.n_out), dtype=torch.float32, device=device) for _ in range(rot)]
+              for _ in range(wl.microbatches)]
+        dxs = [[torch.empty((wl.tokens, lin.k_in), dtype=torch.float32, device=device) for _ in range(rot)]
+               for _ in range(wl.microbatches)]
         epoch = [0]
 
         def step():
+            r = epoch[0] % rot
             refs = []
             for m in range(wl.microbatches):
-                st, ref = ctx.qe_fp8_linear_fwd(0, qe.key(epoch[0], 0, m, 0), xs[m], qe.F32, wl.tokens, ys[m], qe.F32)
+                st, ref = ctx.qe_fp8_linear_fwd(0, qe.key(epoch[0], 0, m, 0), xs[m][r], qe.F32, wl.tokens, ys[m][r],
+                                                qe.F32)
                 assert st == "OK", st
                 refs.append(ref)
             for m in range(wl.microbatches):
-                st = ctx.qe_fp8_linear_dgrad(0, qe.key(epoch[0], 0, m, 0), refs[m], dys[m], qe.F32, dxs[m], qe.F32)
+                st = ctx.qe_fp8_linear_dgrad(0, qe.key(epoch[0], 0, m, 0), refs[m], dys[m][r], qe.F32, dxs[m][r],
+                                             qe.F32)
                 assert st == "OK", st
             for m in range(wl.microbatches):
                 st = ctx.qe_fp8_linear_wgrad_place(0, qe.key(epoch[0], 0, m, 0), refs[m], grad, 0, lin.k_in,
@@ -228,12 +285,20 @@ def per_action_latency(qe, torch, device, steps=200, warmup=10):
         stt = ctx.qe_get_state()
         assert stt["device_token"] == stt["token"]
         res[mode] = el / (steps * 3 * wl.microbatches) * 1e6
+        counters[mode] = {"captures": stt["captures"], "rebinds": stt["rebinds"]}
         ctx.close()
-    return {"workload": wl.key, "actions_per_step": 3 * wl.microbatches,
-            "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
-            "eager_over_graph": round(res["eager"] / res["graph"], 3),
-            "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2),
-            "eager_on_caller_us_per_action": round(res["eager_on_caller"], 2)}
+    out = {"workload": wl.key, "actions_per_step": 3 * wl.microbatches,
+           "graph_us_per_action": round(res["graph"], 2), "eager_us_per_action": round(res["eager"], 2),
+           "eager_over_graph": round(res["eager"] / res["graph"], 3),
+           "graph_on_caller_us_per_action": round(res["graph_on_caller"], 2),
+           "eager_on_caller_us_per_action": round(res["eager_on_caller"], 2)}
+    out["rotating_buffers"] = {
+        "buffer_sets": R, "executor": "replay_on_caller",
+        **{m[len("rotate_"):] + "_us_per_action": round(res[m], 2) for m in res if m.startswith("rotate_")},
+        "graphs_prebuilt": 3 * wl.microbatches,
+        "captures": {m[len("rotate_"):]: counters[m]["captures"] for m in counters if m.startswith("rotate_")},
+        "rebinds": counters["rotate_rebind"]["rebinds"]}
+    return out
 
 
 def wgrad_place(qe, torch, device, tokens=2048, reps=20):
@@ -327,39 +392,91 @@ def qbytes_per_step(wl):
     return q
 
 
-def cpu_baseline(wl, tokens, min_seconds=10.0):
-    """The oracle as it stands, run linear by linear over `tokens` rows (F with
-    the W quantize, dI, dW) until at least `min_seconds` of CPU work is done."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, rows=8192, tokens=4096):
+    """The CPU oracle as it stands, stage by stage, on a bounded sample of the
+    workload: its O projection (K = hidden) restricted to the first `rows`
+    output features of the weight (the first rows of the same seeded draw) at
+    `tokens` tokens, through F (with the weight-cache refresh), dI and dW with
+    INIT placement, each stage timed with perf_counter on the host's cores.
+    `value` is the sample's GEMM FLOPs over the time of all its stages (the
+    headline's definition); the stages report GFLOP/s or GB/s of algorithmic
+    work."""
+    import numpy as np
     import workloads as W
-    from oracle import contract as OC
-    from oracle.layer import Stage
+    from oracle.gemm import gemm_tn, place, quantize_with_amax
+    from oracle.scaling import DelayedScaler
     try:
         from threadpoolctl import threadpool_info
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
-        cores = len(os.sched_getaffinity(0))
-    el, flops, done = 0.0, 0, []
-    for u, lin in enumerate(wl.linears):
-        inp = W.layer_inputs(wl, u, tokens=tokens)
-        w = W.layer_weight(wl, u).as_f32()
+        cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    u = 1
+    lin = wl.linears[u]
+    k, n, t = lin.k_in, min(rows, lin.n_out), min(tokens, wl.tokens)
+    b_in = 2 if wl.in_dtype == "bf16" else 4
+    w = W.normal(W.rng_for(0, wl.cfg, u, W.ROLE_W), (n, k), 0.02, wl.in_dtype).as_f32()
+    inp = W.layer_inputs(wl, u, tokens=t)
+    x = inp["x"].as_f32()
+    dy = np.ascontiguousarray(inp["dy"].as_f32()[:, :n])
+    sx, sw, sdy = (DelayedScaler(f, wl.history, wl.margin) for f in ("E4M3", "E4M3", "E5M2"))
+    stages, tot = [], [0.0]
+
+    def timed(name, fn, work, unit):
         t0 = time.perf_counter()
-        st = Stage(1)
-        st.add_layer(0, u, w, tokens, wl.history, wl.margin)
-        st.add_buffer(4096, lin.n_out * lin.k_in)
-        st.bind(0, 0, 4096, 0, lin.k_in)
-        key = (0, 0, 0, u, 0)
-        s1, y, ref = st.fwd(0, key, inp["x"].as_f32())
-        s2, dx = st.dgrad(0, key, ref, inp["dy"].as_f32())
-        s3 = st.wgrad_place(0, key, ref, 4096, 0, lin.k_in, OC.INIT)
-        el += time.perf_counter() - t0
-        assert s1 == s2 == s3 == OC.OK
-        flops += 3 * 2 * tokens * lin.n_out * lin.k_in
-        done.append(f"{lin.name} {lin.k_in}->{lin.n_out}")
-        if el >= min_seconds:
-            break
-    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{', '.join(done)} at {tokens} tokens: F (with W quantize) + dI + dW through the "
-                      f"float64 oracle, {el:.2f} s"}
+        r = fn()
+        el = time.perf_counter() - t0
+        tot[0] += el
+        rate = work / el / 1e9 if el > 0 else None
+        stages.append({"stage": name, "seconds": round(el, 4), "value": None if rate is None else round(rate, 3),
+                       "unit": unit})
+        return r
+
+    wq, wq_t, a_w = timed("quantize W (cast + transpose + amax)",
+                          lambda: quantize_with_amax(w, sw.scale, "E4M3"), n * k * (b_in + 2), "GB/s")
+    xq, xq_t, a_x = timed("quantize X (cast + transpose + amax)",
+                          lambda: quantize_with_amax(x, sx.scale, "E4M3"), t * k * (b_in + 2), "GB/s")
+    timed("GEMM fwd Y = X W^T", lambda: gemm_tn(xq, "E4M3", wq, "E4M3", sx.scale_inv, sw.scale_inv),
+          2.0 * t * n * k, "GFLOP/s")
+
+    def upd(*ss_amax):
+        for sc, a in ss_amax:
+            if a is not None:
+                sc.record(a)
+            sc.update()
+    t0 = time.perf_counter()
+    upd((sx, a_x), (sw, a_w))
+    el_u = time.perf_counter() - t0
+    dyq, dyq_t, a_dy = timed("quantize dY (cast + transpose + amax)",
+                             lambda: quantize_with_amax(dy, sdy.scale, "E5M2"), t * n * (b_in + 2), "GB/s")
+    timed("GEMM dI dX = dY W", lambda: gemm_tn(dyq, "E5M2", wq_t, "E4M3", sdy.scale_inv, sw.scale_inv),
+          2.0 * t * n * k, "GFLOP/s")
+    t0 = time.perf_counter()
+    upd((sdy, a_dy))
+    el_u += time.perf_counter() - t0
+    tot[0] += el_u
+    stages.append({"stage": "scale updates (X, W, dY)", "seconds": round(el_u, 6),
+                   "us_per_update": round(el_u / 3 * 1e6, 2)})
+    d = timed("GEMM dW = dY^T X", lambda: gemm_tn(dyq_t, "E5M2", xq_t, "E4M3", sdy.scale_inv, sx.scale_inv),
+              2.0 * t * n * k, "GFLOP/s")
+    buf = np.zeros(n * k, dtype=np.float32)
+    timed("placement INIT into the flat FP32 buffer", lambda: place(buf, d, 0, k, accumulate=False), 4.0 * n * k,
+          "GB/s")
+    flops = 3 * 2.0 * t * n * k
+    return {"value": round(flops / tot[0] / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "cpu": cpu_model(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+            "sample": f"{lin.name} {k}->{n} (first {n} of {lin.n_out} output features) at {t} tokens of {wl.key}: "
+                      f"F (with W refresh) + dI + dW through the float64 oracle, {tot[0]:.2f} s",
+            "stages": stages}
 
 
 def progress(msg):
@@ -384,14 +501,19 @@ def main():
         sys.exit(2)
     qe.lib()
     dev = torch.device("cuda:0")
+    torch.zeros(1, device=dev)
+    progress("torch and the library loaded, device initialised")
     wl = W.WORKLOADS[args.workload]
     use_graphs = not args.eager
 
     on_caller = args.executor == "caller"
     b = StageBench(qe, torch, wl, use_graphs, dev, replay_on_caller=on_caller)
+    progress(f"stage registered ({len(wl.linears)} linears); graphs prebuilt in "
+             f"{b.prebuild_ms if b.prebuild_ms is not None else 0:.1f} ms")
     for _ in range(args.warmup):
         b.step()
     torch.cuda.synchronize()
+    progress(f"{args.warmup} warm-up steps done")
     t0 = time.perf_counter()
     for _ in range(args.steps):
         b.step()
@@ -426,7 +548,7 @@ def main():
         import_ms = (time.perf_counter() - t0) * 1e3
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        r.step()                                  # graphs captured again, caches refreshed
+        r.step()                                  # graphs prebuilt again, caches refreshed
         torch.cuda.synchronize()
         first_ms = (time.perf_counter() - t0) * 1e3
         after_ms = timed_ms(r, torch, 0, 3)
@@ -436,7 +558,7 @@ def main():
         assert rst["device_token"] == rst["token"] and rst["e_w"] == epoch + 4
         ckpt = {"payload_bytes": len(payload), "export_ms": round(export_ms, 3), "import_ms": round(import_ms, 3),
                 "first_step_after_restart_ms": round(first_ms, 3), "steady_step_after_restart_ms": round(after_ms, 4),
-                "graph_captures_after_restart": rst["captures"]}
+                "graphs_prebuilt_after_restart_ms": r.prebuild_ms, "graph_captures_after_restart": rst["captures"]}
         r.ctx.close()
         del r
         torch.cuda.empty_cache()
@@ -491,9 +613,31 @@ def main():
         torch.cuda.empty_cache()
         progress("other launch-mode pass")
 
+    # the caller's X / dY / Y / dX buffers rotated over three sets every step
+    # (as a training loop hands the layer new tensors): kernel-node arguments
+    # rewritten in place, the paper's static buffers with copies, re-capture
+    rotation = None
+    if use_graphs and not args.no_rotate:
+        rotation = {"buffer_sets": 3}
+        for name, gi in (("rebind", qe.GRAPH_INPUTS_REBIND), ("copy", qe.GRAPH_INPUTS_COPY),
+                         ("recapture", qe.GRAPH_INPUTS_RECAPTURE)):
+            c = StageBench(qe, torch, wl, True, dev, replay_on_caller=on_caller, graph_inputs=gi, rotate=3)
+            r_ms = timed_ms(c, torch, args.warmup, args.steps)
+            assert c.ctx.qe_sync() == "OK"
+            cst = c.ctx.qe_get_state()
+            assert cst["device_token"] == cst["token"]
+            rotation[name] = {"ms_per_step": round(r_ms, 4), "step_time_vs_headline": round(r_ms / ms, 4),
+                              "captures": cst["captures"], "rebinds": cst["rebinds"],
+                              "capture_ms": round(cst["capture_ns"] / 1e6, 2)}
+            c.ctx.close()
+            del c
+            torch.cuda.empty_cache()
+            progress(f"rotating-buffer pass ({name})")
+
     latency = None if args.no_latency else per_action_latency(qe, torch, dev)
+    progress("per-action latency leg")
     wgrad = None if args.no_wgrad else wgrad_place(qe, torch, dev)
-    progress("latency and dW-placement legs")
+    progress("dW-placement leg")
     torch.cuda.empty_cache()
 
     # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
@@ -552,8 +696,10 @@ def main():
                      "frac": round(q_gbs / HBM_PEAK_GBS, 4), "avg_launch_us": round(q_ms / q_n * 1e3, 2),
                      "launches": q_n},
         "scale_update": {"avg_launch_us": round(u_ms / u_n * 1e3, 2), "launches": u_n},
-        "graph": {"captures": st["captures"], "replays": st["replays"], "handoffs": st["handoffs"],
-                  "capture_ms": round(st["capture_ns"] / 1e6, 2)},
+        "graph": {"graphs_prebuilt": 3 * wl.microbatches * len(wl.linears), "captures": st["captures"],
+                  "replays": st["replays"], "rebinds": st["rebinds"], "handoffs": st["handoffs"],
+                  "prebuild_ms": round(st["prebuild_ns"] / 1e6, 2), "capture_ms": round(st["capture_ns"] / 1e6, 2)},
+        "targets": {"gemm_frac_of_fp8_peak": 0.60, "quantize_amax_wgrad_place_frac_of_hbm": 0.70},
     }
     if copied_ms is not None:
         out["direct_placement_ablation"] = {
@@ -581,12 +727,14 @@ def main():
         out["launch_mode_" + ("direct" if use_graphs else "graph_replay")] = {
             "ms_per_step": round(mode_ms, 4), "value": round(flops / (mode_ms * 1e-3) / 1e12, 2),
             "unit": "TFLOP/s", "step_time_vs_headline": round(mode_ms / ms, 4)}
+    if rotation is not None:
+        out["rotating_buffers"] = rotation
     if latency is not None:
         out["per_action_latency"] = latency
     if wgrad is not None:
         out["wgrad_place"] = wgrad
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(wl)
         progress("cpu baseline")
     print(json.dumps(out), flush=True)
 

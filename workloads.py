@@ -34,17 +34,39 @@ def rng_for(seed: int, cfg: int, unit: int, role: int, mb: int = 0, step: int = 
     return np.random.default_rng(np.random.SeedSequence([seed, cfg, unit, role, mb, step]))
 
 
+def _bf16_chunk(u: np.ndarray, out: np.ndarray) -> None:
+    # u: uint32 bits.  (u + 0x7FFF + lsb) >> 16 cannot wrap in 32 bits for a
+    # non-NaN pattern (the largest, -inf = 0xFF800000, stays far below 2^32);
+    # NaN patterns are replaced afterwards.
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += u
+    r += np.uint32(0x7FFF)
+    r >>= np.uint32(16)
+    nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+    if nan.any():
+        r[nan] = (u[nan] >> np.uint32(16)) | np.uint32(0x40)
+    out[...] = r.astype(np.uint16)
+
+
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 to bfloat16 (RNE on the bit pattern); returns uint16 bits.
 
-    NaN inputs keep a quiet-NaN pattern; infinities pass through."""
+    NaN inputs keep a quiet-NaN pattern; infinities pass through.  Large
+    tensors are converted in chunks on a thread pool (NumPy releases the GIL),
+    which bounds the temporaries to a few chunks."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint32)
-    nan = np.isnan(x)
-    r = np.where(nan, ((u >> 16) | 0x40).astype(np.uint32), r)
-    return r.astype(np.uint16)
+    u = x.reshape(-1).view(np.uint32)
+    out = np.empty(u.shape, dtype=np.uint16)
+    chunk = 1 << 22
+    if u.size <= chunk:
+        _bf16_chunk(u, out)
+    else:
+        from concurrent.futures import ThreadPoolExecutor
+        import os
+        n = max(1, min(16, len(os.sched_getaffinity(0))))
+        with ThreadPoolExecutor(max_workers=n) as ex:
+            list(ex.map(lambda o: _bf16_chunk(u[o:o + chunk], out[o:o + chunk]), range(0, u.size, chunk)))
+    return out.reshape(x.shape)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
