@@ -184,7 +184,8 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
 
 /* Macro-tile shape of every FP8 GEMM the library launches (qe_fp8_gemm_tn and
  * the layer actions).  QE_TILE_AUTO picks, per call, the shape that needs the
- * fewest rounds of workgroups over the 256 compute units, weighted by a
+ * fewest rounds of workgroups over the device's compute units (256 on
+ * MI355X, read from the device properties), weighted by a
  * measured per-round cost; the others force one shape (for tests and
  * measurements).  Process-wide; it applies to launches enqueued afterwards
  * (a graph captured earlier keeps the shapes it was captured with).  The

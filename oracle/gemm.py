@@ -79,13 +79,3 @@ def place(main_grad: np.ndarray, d: np.ndarray, offset: int, ld: int, accumulate
     else:
         main_grad[idx] = d.astype(np.float32)
 
-
-def to_bf16_f32(x) -> np.ndarray:
-    """Round to float32, then to bfloat16 (nearest even); returned as float32.
-
-    The two roundings mirror an FP32 accumulator stored as bf16."""
-    f = np.asarray(x, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    r = (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16).astype(np.uint32)
-    out = r.view(np.float32)
-    return np.where(np.isnan(f), f, out)

@@ -27,7 +27,7 @@
 //    512-byte row runs.  Larger wave tiles mean less LDS traffic per FLOP
 //    than eight waves.
 //  * gemm_tn_kernel, 256 x 128 x 128 tiles: eight waves (two per SIMD) on a
-//    4 x 2 grid; used when it quantizes better onto the 256 CUs.
+//    4 x 2 grid; used when it quantizes better onto the compute units.
 // Operand formats (E4M3 or E5M2) are chosen per call.  K tiles are
 // double-buffered in LDS and filled by LDS-bound global loads
 // (global_load_lds_dwordx4: no register staging, no LDS store instructions)
@@ -65,7 +65,6 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int BK = 128;
 constexpr int kGroupM = 8;
 
-constexpr int kCUs = 256;  // MI355X compute units; one 128 KB-LDS workgroup each
 
 // Cache policy of the epilogue's output traffic (stores, and the destination
 // reads of the accumulate mode): non-temporal.  The output is written once
@@ -750,6 +749,20 @@ constexpr double kCost224 = 0.98;
 
 static std::atomic<int> g_tile_override{0};
 
+// Compute units of the current device (one 128 KB-LDS workgroup each at a
+// time), read once per device from its properties; 256 on MI355X.
+static int cu_count() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
 hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
   // The kernel addresses each operand with 32-bit offsets: split any operand
@@ -785,9 +798,10 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   // win where the 256 x 256 grid leaves its last round mostly empty (N = 6144:
   // 384 tiles = 1.5 rounds, against 512 tiles of 256 x 192 = 2 rounds of 0.89;
   // N = 14336: 896 tiles = 3.5 rounds, against 1024 of 256 x 224 = 4 of 0.98).
+  const int64_t cus = cu_count();
   auto rounds = [&](int64_t bm, int64_t bn) {
     const int64_t t = ((g.m + bm - 1) / bm) * ((g.n + bn - 1) / bn);
-    return double((t + kCUs - 1) / kCUs);
+    return double((t + cus - 1) / cus);
   };
   const int force = g_tile_override.load(std::memory_order_relaxed);
   const double c256 = rounds(256, 256);

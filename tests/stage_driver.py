@@ -10,19 +10,24 @@ from tests.gpu_util import dev_bytes, dev_f32, torch, upload
 
 class Spec:
     def __init__(self, shapes, tokens, M, history, margin, in_dtype, shared_view, out_dtype="f32", seed=0,
-                 cfg=90, outliers=False, scaling="delayed", w_dtype=None, fmt_w="E4M3"):
-        """`w_dtype`: the master weights' dtype (default `in_dtype`); `fmt_w`: W's FP8 format."""
+                 cfg=90, outliers=False, scaling="delayed", w_dtype=None, fmt_w="E4M3", ld_pad=0):
+        """`w_dtype`: the master weights' dtype (default `in_dtype`); `fmt_w`: W's FP8 format;
+        `ld_pad`: each gradient view's row stride is K + ld_pad (elements between rows untouched)."""
+        self.ld_pad = ld_pad
         self.shapes, self.tokens, self.M = shapes, tokens, M
         self.w_dtype, self.fmt_w = w_dtype or in_dtype, fmt_w
         self.history, self.margin, self.in_dtype = history, margin, in_dtype
         self.shared_view, self.out_dtype, self.seed, self.cfg = shared_view, out_dtype, seed, cfg
         self.outliers, self.scaling = outliers, scaling
 
+    def ld(self, u):
+        return self.shapes[u][1] + self.ld_pad
+
     def total(self):
-        return sum(n * k for n, k in self.shapes)
+        return sum(n * self.ld(u) for u, (n, k) in enumerate(self.shapes))
 
     def offset(self, u, m):
-        offs = np.cumsum([0] + [n * k for n, k in self.shapes])
+        offs = np.cumsum([0] + [n * self.ld(v) for v, (n, k) in enumerate(self.shapes)])
         return int(offs[u] if self.shared_view else m * self.total() + offs[u])
 
     def grad_elems(self):
@@ -71,7 +76,8 @@ class GpuStage:
         self.grad = torch.zeros(spec.grad_elems(), dtype=torch.float32, device=self.d)
         for u, (n, k) in enumerate(spec.shapes):
             for m in range(spec.M):
-                assert self.ctx.qe_arena_bind(u, m, self.grad, spec.grad_elems(), spec.offset(u, m), k) == "OK"
+                assert self.ctx.qe_arena_bind(u, m, self.grad, spec.grad_elems(), spec.offset(u, m),
+                                              spec.ld(u)) == "OK"
         self.refs = {}
         self.written = set()
         self.outs = {}
@@ -122,13 +128,13 @@ class GpuStage:
         elif a == "dW":
             mode = self._mode(u, m)
             st = self.ctx.qe_fp8_linear_wgrad_place(u, key, self.refs[(u, m)], self.grad, spec.offset(u, m),
-                                                    k, mode, caller=caller)
+                                                    spec.ld(u), mode, caller=caller)
             self.written.add((u, spec.offset(u, m)))
         else:
             dx = self._out(spec.tokens, k)
             mode = self._mode(u, m)
             st = self.ctx.qe_fp8_linear_bwd_full(u, key, self.refs[(u, m)], upload(dy, self.d), dt, dx, odt,
-                                                 self.grad, spec.offset(u, m), k, mode, caller=caller)
+                                                 self.grad, spec.offset(u, m), spec.ld(u), mode, caller=caller)
             self.written.add((u, spec.offset(u, m)))
             self.outs[("dx", u, m, step)] = dx
         assert st == "OK", (a, m, u, st)
@@ -183,7 +189,7 @@ class OracleStage:
         self.st.add_buffer(self.buf, spec.grad_elems())
         for u, (n, k) in enumerate(spec.shapes):
             for m in range(spec.M):
-                assert self.st.bind(u, m, self.buf, spec.offset(u, m), k) == OC.OK
+                assert self.st.bind(u, m, self.buf, spec.offset(u, m), spec.ld(u)) == OC.OK
         self.refs = {}
         self.outs = {}
 
@@ -204,11 +210,11 @@ class OracleStage:
                 elif a == "dI":
                     st, self.outs[("dx", u, m, step)] = self.st.dgrad(u, key, self.refs[(u, m)], dy.as_f32())
                 elif a == "dW":
-                    st = self.st.wgrad_place(u, key, self.refs[(u, m)], self.buf, spec.offset(u, m), k,
+                    st = self.st.wgrad_place(u, key, self.refs[(u, m)], self.buf, spec.offset(u, m), spec.ld(u),
                                              self._mode(u, m))
                 else:
                     st, self.outs[("dx", u, m, step)] = self.st.bwd_full(u, key, self.refs[(u, m)], dy.as_f32(),
-                                                                         self.buf, spec.offset(u, m), k,
+                                                                         self.buf, spec.offset(u, m), spec.ld(u),
                                                                          self._mode(u, m))
                 assert st == OC.OK, (a, m, u, st)
 
@@ -221,7 +227,7 @@ class OracleStage:
             acc = np.zeros((n, k), dtype=np.float64)
             for m in range(1 if spec.shared_view else spec.M):
                 o = spec.offset(u, m)
-                acc += g[o:o + n * k].reshape(n, k)
+                acc += g[o:o + n * spec.ld(u)].reshape(n, spec.ld(u))[:, :k]
             w = (self.st.layers[u].w.astype(np.float64) - lr * acc).astype(np.float32)
             t = W.Tensor(W.f32_to_bf16_bits(w), "bf16") if spec.w_dtype == "bf16" else W.Tensor(w, "f32")
             new.append(t)

@@ -117,17 +117,18 @@ def dw_block(x, dy, xs, dys, J, Kk):
 
 
 # ---------------------------------------------------------------------------------------- ZB
-@pytest.mark.timeout(600)
+@pytest.mark.timeout(900)
 def test_zero_bubble_8x2048_fullsize():
+    """Three optimizer steps (24 updates per role against a 16-entry history, so
+    the first amaxes age out in the third step), new inputs every step, microbatch
+    0's activations of the first step scaled by 8 (exact in bf16) so that their
+    amax dominates the window until it is evicted: the X scale then rises again.
+    FP32 outputs in steps 0 and 2 (held to 1e-3), bf16 in step 1."""
     qe = need_lib()
     d = dev()
     wl = W.WORKLOADS["llama3_8b_zb_8x2048"]
-    M, t = wl.microbatches, wl.tokens
-    print("zb: generating inputs", flush=True)
-    ws = [W.layer_weight(wl, u) for u in range(len(wl.linears))]
-    inp = {(u, m): W.layer_inputs(wl, u, mb=m) for u in range(len(wl.linears)) for m in range(M)}
-    amax_x = {k: amax_of(v["x"]) for k, v in inp.items()}
-    amax_dy = {k: amax_of(v["dy"]) for k, v in inp.items()}
+    M, t, L = wl.microbatches, wl.tokens, len(wl.linears)
+    ws = [W.layer_weight(wl, u) for u in range(L)]
     ctx = qe.Context(M, use_graphs=True)
     dw_dev = [upload(w, d) for w in ws]
     offs = wl.grad_offsets()
@@ -136,27 +137,35 @@ def test_zero_bubble_8x2048_fullsize():
         assert ctx.qe_layer_register(0, u, lin.n_out, lin.k_in, t, dw_dev[u], qe.BF16, wl.history, wl.margin)[0] == "OK"
         for m in range(M):                 # one shared view per linear: microbatches accumulate
             assert ctx.qe_arena_bind(u, m, grad, grad.numel(), offs[u], lin.k_in) == "OK"
-    x_dev = {k: upload(v["x"], d) for k, v in inp.items()}
-    dy_dev = {k: upload(v["dy"], d) for k, v in inp.items()}
-    outs = {(u, m): (torch.empty((t, lin.n_out), dtype=torch.int16, device=d),
-                     torch.empty((t, lin.k_in), dtype=torch.int16, device=d))
-            for u, lin in enumerate(wl.linears) for m in range(M)}
-    tr = Tracker(len(wl.linears), wl.history, wl.margin)
+    tr = Tracker(L, wl.history, wl.margin)
     rng = np.random.default_rng(7)
-    for step, sched in enumerate([S.ZB_STEP0, S.ZB_STEP1]):
-        print(f"zb: step {step}", flush=True)
+    scales_x = []
+    for step, sched in enumerate([S.ZB_STEP0, S.ZB_STEP1, S.ZB_STEP0]):
+        print(f"zb: step {step}: generating inputs", flush=True)
+        inp = {(u, m): W.layer_inputs(wl, u, mb=m, step=step) for u in range(L) for m in range(M)}
+        if step == 0:
+            for u in range(L):
+                x = inp[(u, 0)]["x"]
+                inp[(u, 0)]["x"] = W.Tensor(W.f32_to_bf16_bits(f32_of(x) * np.float32(8.0)), "bf16")
+        amax_x = {k: amax_of(v["x"]) for k, v in inp.items()}
+        amax_dy = {k: amax_of(v["dy"]) for k, v in inp.items()}
+        x_dev = {k: upload(v["x"], d) for k, v in inp.items()}
+        dy_dev = {k: upload(v["dy"], d) for k, v in inp.items()}
+        odt, tdt = (qe.BF16, torch.int16) if step == 1 else (qe.F32, torch.float32)
+        outs = {(u, m): (torch.empty((t, lin.n_out), dtype=tdt, device=d),
+                         torch.empty((t, lin.k_in), dtype=tdt, device=d))
+                for u, lin in enumerate(wl.linears) for m in range(M)}
+        print(f"zb: step {step}: running", flush=True)
         S.check_legal(sched, M)
-        refs, written, dw_order = {}, set(), {u: [] for u in range(len(wl.linears))}
+        refs, written, dw_order = {}, set(), {u: [] for u in range(L)}
         for a, m in sched:
             for u, lin in enumerate(wl.linears):
                 key = qe.key(step, 0, m, u)
                 if a == "F":
-                    st, refs[(u, m)] = ctx.qe_fp8_linear_fwd(u, key, x_dev[(u, m)], qe.BF16, t, outs[(u, m)][0],
-                                                             qe.BF16)
+                    st, refs[(u, m)] = ctx.qe_fp8_linear_fwd(u, key, x_dev[(u, m)], qe.BF16, t, outs[(u, m)][0], odt)
                     tr.fwd(u, m, step, amax_x[(u, m)], amax_of(ws[u]) if m == 0 else None)
                 elif a == "dI":
-                    st = ctx.qe_fp8_linear_dgrad(u, key, refs[(u, m)], dy_dev[(u, m)], qe.BF16, outs[(u, m)][1],
-                                                 qe.BF16)
+                    st = ctx.qe_fp8_linear_dgrad(u, key, refs[(u, m)], dy_dev[(u, m)], qe.BF16, outs[(u, m)][1], odt)
                     tr.dgrad(u, m, step, amax_dy[(u, m)])
                 else:
                     mode = qe.ACCUM if u in written else qe.INIT
@@ -165,6 +174,7 @@ def test_zero_bubble_8x2048_fullsize():
                     dw_order[u].append(m)
                 assert st == "OK", (a, m, u, st)
         torch.cuda.synchronize()
+        scales_x.append([tr.fwd_used[(0, m, step)][0] for m in range(M)])
         for u, lin in enumerate(wl.linears):
             n, k = lin.n_out, lin.k_in
             tr.check_state(qe, ctx, d, u)
@@ -184,14 +194,19 @@ def test_zero_bubble_8x2048_fullsize():
             g = grad.cpu().numpy()
             assert rel_err(g[offs[u] + J[:, None] * k + Kk[None, :]], ref) <= 1e-3, (u, step)
         assert ctx.qe_arena_finalize() == "OK"
-        if step == 0:                      # optimizer step: W <- bf16(0.75 W), in place
-            for u in range(len(wl.linears)):
+        if step < 2:                       # optimizer step: W <- bf16(0.75 W), in place
+            for u in range(L):
                 ws[u] = W.Tensor(W.f32_to_bf16_bits(f32_of(ws[u]) * np.float32(0.75)), "bf16")
                 dw_dev[u].copy_(upload(ws[u], d))
         assert ctx.qe_optimizer_commit() == "OK"
+        del inp, x_dev, dy_dev, outs
     assert ctx.qe_sync() == "OK"
     st = ctx.qe_get_state()
-    assert st["device_token"] == st["token"] == 2 * 2 * M * len(wl.linears)
+    assert st["device_token"] == st["token"] == 3 * 2 * M * L
+    # the scaled amax (update 1) holds the X scale down through update 16; from update 18 on
+    # (step 2, microbatch 1: the first cast after the 17th update) it has aged out
+    assert scales_x[1][-1] == scales_x[0][1] == scales_x[2][0]
+    assert scales_x[2][1] > scales_x[1][-1]
     ctx.close()
 
 
@@ -274,6 +289,7 @@ def test_llama3_70b_stage_100_replays():
         assert ctx.qe_arena_bind(u, 0, grad, grad.numel(), offs[u], lin.k_in) == "OK"
         outs.append((torch.empty((t, lin.n_out), dtype=torch.int16, device=d),
                      torch.empty((t, lin.k_in), dtype=torch.int16, device=d)))
+    assert ctx.qe_prebuild_graphs(t, qe.BF16, qe.BF16, qe.BF16, qe.BF16) == "OK"   # as the bench does
     tr = Tracker(len(wl.linears), wl.history, wl.margin)
     snap = None
     steps = 100
@@ -301,6 +317,7 @@ def test_llama3_70b_stage_100_replays():
     st = ctx.qe_get_state()
     assert st["device_token"] == st["token"] == 2 * steps * len(wl.linears)
     assert st["replays"] == 3 * steps * len(wl.linears)
+    assert st["captures"] == 3 * len(wl.linears)     # the prebuilt graphs only
     # every replay after the scales settled reproduces step 1 bit for bit
     for (y1, dx1), (y, dx) in zip(snap[0], outs):
         assert torch.equal(y1, y) and torch.equal(dx1, dx)
@@ -318,4 +335,99 @@ def test_llama3_70b_stage_100_replays():
         check_cache(ctx, d, u, w, tr.w_scale[u][0], J, n, k)
         check_y_dx(outs[u][0], outs[u][1], x, dy, w, xs, tr.w_scale[u], dys, I, J, Kk)
         assert rel_err(g[offs[u] + J[:, None] * k + Kk[None, :]], dw_block(x, dy, xs, dys, J, Kk)) <= 1e-3
+    # one more step with FP32 outputs, held to 1e-3 (graphs captured for the new output dtype)
+    del snap, outs
+    torch.cuda.empty_cache()
+    outs32 = [(torch.empty((t, lin.n_out), dtype=torch.float32, device=d),
+               torch.empty((t, lin.k_in), dtype=torch.float32, device=d)) for lin in wl.linears]
+    refs = []
+    for u in range(len(wl.linears)):
+        st, ref = ctx.qe_fp8_linear_fwd(u, qe.key(steps, 0, 0, u), devs[u][1], qe.BF16, t, outs32[u][0], qe.F32)
+        assert st == "OK"
+        tr.fwd(u, 0, steps, host[u][4], host[u][3])
+        refs.append(ref)
+    for u in reversed(range(len(wl.linears))):
+        key = qe.key(steps, 0, 0, u)
+        assert ctx.qe_fp8_linear_dgrad(u, key, refs[u], devs[u][2], qe.BF16, outs32[u][1], qe.F32) == "OK"
+        tr.dgrad(u, 0, steps, host[u][5])
+        assert ctx.qe_fp8_linear_wgrad_place(u, key, refs[u], grad, offs[u], wl.linears[u].k_in, qe.INIT) == "OK"
+    torch.cuda.synchronize()
+    g = grad.cpu().numpy()
+    for u, lin in enumerate(wl.linears):
+        n, k = lin.n_out, lin.k_in
+        tr.check_state(qe, ctx, d, u)
+        w, x, dy = host[u][0], host[u][1], host[u][2]
+        xs, dys = tr.fwd_used[(u, 0, steps)], tr.dgrad_used[(u, 0, steps)]
+        I = np.sort(rng.choice(t, 16, replace=False))
+        J = np.sort(rng.choice(n, 16, replace=False))
+        Kk = np.sort(rng.choice(k, 16, replace=False))
+        check_y_dx(outs32[u][0], outs32[u][1], x, dy, w, xs, tr.w_scale[u], dys, I, J, Kk)
+        assert rel_err(g[offs[u] + J[:, None] * k + Kk[None, :]], dw_block(x, dy, xs, dys, J, Kk)) <= 1e-3
     ctx.close()
+
+
+# ---------------------------------------------------------------------------------------- outlier age-out
+@pytest.mark.timeout(600)
+def test_outlier_8192cube_ages_out_with_history_4():
+    """The outlier-stress shape with a 4-entry history: a clean step, one step
+    with the outlier activations and log-normal gradients, then clean steps.
+    The outlier step's amax lowers the X and dY scales for exactly four
+    updates, then ages out and the scales rise back to their clean values;
+    every history and scale bit-exact against the oracle's, codes and products
+    checked on sampled rows / columns at the outlier step and after it."""
+    qe = need_lib()
+    d = dev()
+    wl = W.WORKLOADS["outlier_8192cube"]
+    lin = wl.linears[0]
+    n, k, t = lin.n_out, lin.k_in, wl.tokens
+    H = 4
+    w = W.layer_weight(wl, 0)
+    clean = W.layer_inputs(wl, 0, outliers=False)
+    hot = W.layer_inputs(wl, 0, outliers=True)
+    am = {name: (amax_of(v["x"]), amax_of(v["dy"])) for name, v in (("clean", clean), ("hot", hot))}
+    ctx = qe.Context(1, use_graphs=True, replay_on_caller=True)
+    w_dev = upload(w, d)
+    dev_in = {name: (upload(v["x"], d), upload(v["dy"], d)) for name, v in (("clean", clean), ("hot", hot))}
+    assert ctx.qe_layer_register(0, 0, n, k, t, w_dev, qe.F32, H, wl.margin)[0] == "OK"
+    grad = torch.zeros(n * k, dtype=torch.float32, device=d)
+    assert ctx.qe_arena_bind(0, 0, grad, grad.numel(), 0, k) == "OK"
+    y = torch.empty((t, n), dtype=torch.float32, device=d)
+    dx = torch.empty((t, k), dtype=torch.float32, device=d)
+    tr = Tracker(1, H, wl.margin)
+    rng = np.random.default_rng(11)
+    a_w = amax_of(w)
+    plan = ["clean", "hot"] + ["clean"] * 6
+    used = []
+    for step, which in enumerate(plan):
+        key = qe.key(step, 0, 0, 0)
+        xd, dyd = dev_in[which]
+        st, ref = ctx.qe_fp8_linear_fwd(0, key, xd, qe.F32, t, y, qe.F32)
+        assert st == "OK"
+        tr.fwd(0, 0, step, am[which][0], a_w)
+        assert ctx.qe_fp8_linear_dgrad(0, key, ref, dyd, qe.F32, dx, qe.F32) == "OK"
+        tr.dgrad(0, 0, step, am[which][1])
+        assert ctx.qe_fp8_linear_wgrad_place(0, key, ref, grad, 0, k, qe.INIT) == "OK"
+        torch.cuda.synchronize()
+        tr.check_state(qe, ctx, d, 0)
+        xs, dys = tr.fwd_used[(0, 0, step)], tr.dgrad_used[(0, 0, step)]
+        used.append((xs[0], dys[0]))
+        if which == "hot" or step in (2, 6):
+            src = hot if which == "hot" else clean
+            I = np.sort(rng.choice(t, 16, replace=False))
+            J = np.sort(rng.choice(n, 16, replace=False))
+            big = np.argsort(-np.abs(f32_of(src["x"], rows=np.arange(0, t, 512))).max(0))[:8]
+            Kk = np.unique(np.concatenate([big, rng.choice(k, 16, replace=False)]))
+            p = ctx.qe_layer_slot_payload(0, 0)
+            xt = dev_bytes(p["x_q_t"], k * p["ld_x_q_t"], d).reshape(k, p["ld_x_q_t"])[:, :t]
+            np.testing.assert_array_equal(xt[Kk], gemm.quantize(f32_of(src["x"], cols=Kk).T, xs[0], "E4M3"))
+            check_y_dx(y, dx, src["x"], src["dy"], w, xs, tr.w_scale[0], dys, I, J, Kk)
+            g = grad.cpu().numpy()
+            assert rel_err(g[J[:, None] * k + Kk[None, :]], dw_block(src["x"], src["dy"], xs, dys, J, Kk)) <= 1e-3
+        assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+    ctx.close()
+    # casts of step s use the scale after update s: the hot amax (update 2) is in
+    # the window for updates 2..5, so steps 2..5 cast with the lowered scale and
+    # step 6 with the clean one again
+    assert used[2][0] < used[1][0] and used[2][1] < used[1][1]
+    assert all(used[s] == used[2] for s in (3, 4, 5))
+    assert used[6] == used[1] == used[7]

@@ -134,3 +134,44 @@ def test_amax_accumulates_and_nan_propagates():
     assert qe.qe_quantize_fp8(c, qe.F32, 1, 2, m) == "OK"
     torch.cuda.synchronize()
     assert math.isnan(mb[0].item())
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("fmt", ["E4M3", "E5M2"])
+@pytest.mark.parametrize("shape", [(256, 384), (37, 53)], ids=["full_tiles", "ragged"])
+def test_subnormal_inputs_scaled_to_normal(dtype, fmt, shape):
+    """An all-subnormal tensor (FP32 / BF16 subnormals, both signs, with zeros):
+    the scale update clamps its exponent to 126, and the cast multiplies every
+    subnormal input by 2^126, which lands in the normal range; codes and the
+    recorded amax must match the oracle bit for bit (a flush of subnormal
+    inputs to zero would make every code zero)."""
+    qe = need_lib()
+    d = dev()
+    rng = np.random.default_rng(5)
+    mant = rng.integers(0, 1 << 23, size=shape, dtype=np.int64).astype(np.uint32)
+    if dtype == "bf16":
+        mant &= np.uint32(0x007F0000)            # bf16 subnormals: the top 7 mantissa bits
+    sign = rng.integers(0, 2, size=shape, dtype=np.int64).astype(np.uint32) << 31
+    bits = (sign | mant).astype(np.uint32)
+    x = bits.view(np.float32)
+    assert not np.any(np.isfinite(x) & (np.abs(x) >= np.float32(2.0 ** -126)))
+    t = W.Tensor((bits >> 16).astype(np.uint16), "bf16") if dtype == "bf16" else W.Tensor(x, "f32")
+    x_f32 = t.as_f32()
+    f = qe.E4M3 if fmt == "E4M3" else qe.E5M2
+    # the exponent the scale update derives from this amax, clamped to 126
+    a = scaling.amax(x_f32)
+    assert 0.0 < a < 2.0 ** -126
+    assert scaling.scale_exponent(a, fmt, 0) == 126
+    H = 4
+    mb = meta_buffer(H, d, 1.0)
+    meta = meta_of(qe, mb, f)
+    # first cast at scale 1 records the amax; the update sets scale = 2^126
+    qr, qc, mb1, snap = run_quant(qe, d, t, f, 1.0, H=H)
+    mb.copy_(torch.from_numpy(mb1).to(d))
+    assert qe.qe_amax_scale_update([meta]) == "OK"
+    torch.cuda.synchronize()
+    m = mb.cpu().numpy()
+    assert m[H] == np.float32(2.0 ** 126) and m[H + 1] == np.float32(2.0 ** -126)
+    qr, qc, _, snap = run_quant(qe, d, t, f, 2.0 ** 126, H=H)
+    check(x_f32, fmt, qr, qc, mb1, snap, 2.0 ** 126)
+    assert np.count_nonzero(qr) > qr.size // 2
