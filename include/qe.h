@@ -165,6 +165,30 @@ qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t row
                                   int64_t ld_col, float *scale_inv_snapshot, int64_t *device_token,
                                   qe_stream stream);
 
+/* Allocation-free variant of qe_quantize_fp8_current, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same cast with the same results, but
+ * the amax accumulator (the per-line partial maxima the amax pass folds its
+ * workgroups into) is a scratch array inside the library, 16 KiB per device
+ * and held by each device the library runs on until the process ends,
+ * instead of one the caller brings in meta_host->amax_accum, which must be
+ * NULL here.  The call allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine); the first call on a device looks up that device's copy of
+ * the scratch.  Four launches on `stream`: a kernel clears the scratch, then
+ * qe_quantize_fp8_current's amax pass, scale update and cast.  The scratch
+ * size does not depend on the tensor (any number of workgroups folds into its
+ * 64 lines), so every size qe_quantize_fp8_current accepts is accepted.
+ * Every call on one device shares that device's scratch: calls that overlap
+ * on one device (on different streams, or from different host threads
+ * without ordering) race and give undefined results; calls ordered on one
+ * stream are independent.  Other arguments and errors as for
+ * qe_quantize_fp8_current; QE_ERR_INVALID_ARG also when
+ * meta_host->amax_accum is set; QE_ERR_HIP if the scratch cannot be found. */
+qe_status qe_quantize_fp8_current_noalloc(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols,
+                                          const qe_fp8_meta *meta_host, uint8_t *q_row, int64_t ld_row,
+                                          uint8_t *q_col, int64_t ld_col, float *scale_inv_snapshot,
+                                          int64_t *device_token, qe_stream stream);
+
 /* FP8 GEMM in "TN" form (both operands contiguous along the reduction axis):
  *     D[i][j] = (a_scale_inv * b_scale_inv) * sum_r A[i][r] * B[j][r]
  * A: m x k codes of format fmt_a, row stride lda bytes.  B: n x k codes of

@@ -80,7 +80,19 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(AmaxParams p) {
   }
 }
 
+__global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n; i += int64_t(gridDim.x) * kThreads)
+    p[i] = 0.0f;
+}
+
 }  // namespace
+
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 1024) blocks = 1024;
+  return klaunch(fill_zero_kernel, dim3(unsigned(blocks)), dim3(kThreads), 0, s, p, n);
+}
 
 hipError_t launch_amax(const AmaxParams &p, hipStream_t s) {
   if (p.nvec == 0 && p.head + p.tail == 0) return hipSuccess;  // empty tensor: amax 0, nothing to fold

@@ -31,6 +31,7 @@
 
 #include <chrono>
 #include <map>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -38,9 +39,33 @@
 #include "contract.h"
 #include "kernels.h"
 
+// Scratch of qe_quantize_fp8_current_noalloc: one amax accumulator
+// (kAmaxLines lines, kAmaxStride floats apart: 16 KiB), one copy per device,
+// held until the process ends.  In host code this name is a host-side stand-in:
+// the device address comes from hipGetSymbolAddress (noalloc_scratch below).
+static __device__ __align__(256) float scratch[qe::kAmaxLines * qe::kAmaxStride];
+
 namespace {
 
 int64_t rup16(int64_t v) { return (v + 15) / 16 * 16; }
+
+// Device address of `scratch` on the current device, looked up once per
+// device (each device holds its own copy at its own address).
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_ptr[kScratchDevices] = {};
+
+float *noalloc_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+    g_scratch_ptr[dev] = static_cast<float *>(p);
+  }
+  return g_scratch_ptr[dev];
+}
 
 // Makes the context's device current for the scope of one call and restores
 // the caller's device afterwards.
@@ -747,6 +772,37 @@ qe_status qe_quantize_fp8_current(const void *in, qe_dtype in_dtype, int64_t row
   u.token = reinterpret_cast<long long *>(device_token);
   const Call q = quant_call(in, in_dtype, rows, cols, m, q_row, ld_row, q_col, ld_col, scale_inv_snapshot, false);
   if (qe::launch_amax(a.a, s) != hipSuccess || qe::launch_scale_update(u, s) != hipSuccess ||
+      qe::launch_quantize(q.q, s) != hipSuccess)
+    return QE_ERR_HIP;
+  return QE_OK;
+}
+
+qe_status qe_quantize_fp8_current_noalloc(const void *in, qe_dtype in_dtype, int64_t rows, int64_t cols,
+                                          const qe_fp8_meta *meta_host, uint8_t *q_row, int64_t ld_row,
+                                          uint8_t *q_col, int64_t ld_col, float *scale_inv_snapshot,
+                                          int64_t *device_token, qe_stream stream) {
+  if (!valid_dtype(in_dtype) || rows < 0 || cols < 0 || !meta_ok(meta_host) || meta_host->history_len != 1 ||
+      meta_host->amax_accum != nullptr)
+    return QE_ERR_INVALID_ARG;
+  if (rows > 0 && cols > 0 && in == nullptr) return QE_ERR_INVALID_ARG;
+  if (q_row != nullptr && ld_row < cols) return QE_ERR_INVALID_ARG;
+  if (q_col != nullptr && ld_col < rows) return QE_ERR_INVALID_ARG;
+  if (uintptr_t(in) % (in_dtype == QE_BF16 ? 2 : 4) != 0) return QE_ERR_INVALID_ARG;
+  float *acc = noalloc_scratch();
+  if (acc == nullptr) return QE_ERR_HIP;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  qe::MetaRef m = meta_ref(*meta_host);
+  m.accum = acc;  // the amax pass folds into the scratch accumulator; the update folds and clears it
+  const Call a = amax_call(in, in_dtype, rows * cols, m);
+  qe::UpdateParams u;
+  memset(&u, 0, sizeof(u));
+  u.m[0] = m;
+  u.n = 1;
+  u.token = reinterpret_cast<long long *>(device_token);
+  const Call q = quant_call(in, in_dtype, rows, cols, m, q_row, ld_row, q_col, ld_col, scale_inv_snapshot, false);
+  // the scratch keeps the last call's contents: cleared first, by a kernel
+  if (qe::launch_fill_zero(acc, int64_t(qe::kAmaxLines) * qe::kAmaxStride, s) != hipSuccess ||
+      qe::launch_amax(a.a, s) != hipSuccess || qe::launch_scale_update(u, s) != hipSuccess ||
       qe::launch_quantize(q.q, s) != hipSuccess)
     return QE_ERR_HIP;
   return QE_OK;

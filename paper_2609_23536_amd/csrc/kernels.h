@@ -170,6 +170,8 @@ hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
 void set_gemm_tile_override(int tile);
 hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s);
 hipError_t launch_amax(const AmaxParams &p, hipStream_t s);
+// p[0..n) = 0 with a kernel (no memset node when captured into a graph)
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
 AmaxParams amax_params(const void *in, bool bf16, int64_t numel, float *amax, float *accum);
 
 }  // namespace qe

@@ -92,6 +92,7 @@ _SIGS = {
     "qe_quantize_fp8": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P],
     "qe_amax": [_P, _I32, _I64, C.POINTER(FP8Meta), _P],
     "qe_quantize_fp8_current": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P, _P],
+    "qe_quantize_fp8_current_noalloc": [_P, _I32, _I64, _I64, C.POINTER(FP8Meta), _P, _I64, _P, _I64, _P, _P, _P],
     "qe_fp8_gemm_tn": [_P, _I32, _I64, _P, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _I32, _I64, _I32, _P],
     "qe_set_gemm_tile": [_I32],
     "qe_ctx_create": [C.POINTER(Config), C.POINTER(_P)],
@@ -197,6 +198,14 @@ def qe_quantize_fp8_current(inp, in_dtype: int, rows: int, cols: int, meta: FP8M
     return _st(lib().qe_quantize_fp8_current(ptr(inp), in_dtype, rows, cols, C.byref(meta), ptr(q_row), ld_row,
                                              ptr(q_col), ld_col, ptr(scale_inv_snapshot), ptr(device_token),
                                              stream_handle(stream)))
+
+
+def qe_quantize_fp8_current_noalloc(inp, in_dtype: int, rows: int, cols: int, meta: FP8Meta, q_row=None,
+                                    ld_row: int = 0, q_col=None, ld_col: int = 0, scale_inv_snapshot=None,
+                                    device_token=None, stream=None) -> str:
+    return _st(lib().qe_quantize_fp8_current_noalloc(ptr(inp), in_dtype, rows, cols, C.byref(meta), ptr(q_row),
+                                                     ld_row, ptr(q_col), ld_col, ptr(scale_inv_snapshot),
+                                                     ptr(device_token), stream_handle(stream)))
 
 
 def qe_fp8_gemm_tn(a, fmt_a: int, lda: int, b, fmt_b: int, ldb: int, m: int, n: int, k: int, a_scale_inv,
