@@ -282,26 +282,41 @@ typedef struct {
   int32_t scaling;       /* qe_scaling; QE_SCALING_CURRENT requires history_len == 1 */
 } qe_layer_desc;
 
-/* Create a context.  Allocates the graph stream and events (unless
- * null_executor).  Errors: QE_ERR_INVALID_ARG (also replay_on_caller outside
- * {0, 1}, or together with one_way_handoff), QE_ERR_UNSUPPORTED, QE_ERR_HIP. */
+/* Create a context: one pipeline stage's executor and contract state (§4.1,
+ * Algorithm 1, whose state starts at e_W = 0, token 0, every slot free at
+ * generation 0; §4.4 for the one stream-ordered graph stream).  Allocates the
+ * graph stream and events (unless null_executor, the host-only mode of the
+ * CPU fault injections of §5.2).  Errors: QE_ERR_INVALID_ARG (also
+ * replay_on_caller outside {0, 1}, or together with one_way_handoff, or
+ * graph_inputs outside its enum), QE_ERR_UNSUPPORTED, QE_ERR_HIP. */
 qe_status qe_ctx_create(const qe_config *cfg_host, qe_ctx **out_host);
+/* Destroy a context: waits for its device work, then frees its graphs,
+ * events, streams and every allocation of its layers.  NULL is a no-op. */
 void qe_ctx_destroy(qe_ctx *ctx);
 
-/* Register a linear layer.  Allocates its FP8 state (three roles), its
- * quantized-weight cache W_q [N,K] and W_q^T [K,N], one tape payload per slot
- * (X_q^T [K, tokens], dY_q^T [N, tokens] and the two scale_inv snapshots),
- * and scratch for the row-wise X_q / dY_q.  (stage, unit) must be unique.
+/* Register a linear layer: one sub-layer unit u of the stage, the (s, u)
+ * part of every TapeKey of its actions (§3.1), with the delayed-scaling state
+ * S of its three tensor roles (§2.1, §3.2), its weight cache and version
+ * e_C (§3.3) and one tape slot per configured microbatch (§4.3: static
+ * binding, one slot per microbatch).  Allocates its FP8 state (three roles),
+ * its quantized-weight cache W_q [N,K] and W_q^T [K,N], one tape payload per
+ * slot (X_q^T [K, tokens], dY_q^T [N, tokens] and the two scale_inv
+ * snapshots: the retained Q_m of §3.2), and scratch for the row-wise X_q /
+ * dY_q.  (stage, unit) must be unique (QE_ERR_INVALID_ARG); so must be the
+ * bounds: 1 <= history_len <= 8192, formats and dtypes in their enums.
  * With desc->scaling == QE_SCALING_CURRENT every cast below takes its scale
  * from the amax of the tensor it casts (qe_quantize_fp8_current's sequence)
  * instead of from the history; nothing else about the actions changes. */
 qe_status qe_layer_register(qe_ctx *ctx, const qe_layer_desc *desc_host, int32_t *layer_out_host);
 
-/* Device pointers of a role's FP8 state (for inspection / checkpointing). */
+/* Device pointers of a role's FP8 state S (§2.1: amax history, scale,
+ * scale_inv; §3.5: the part of the state a checkpoint persists), for
+ * inspection.  Errors: QE_ERR_INVALID_ARG for a bad layer or role. */
 qe_status qe_layer_meta(const qe_ctx *ctx, int32_t layer, qe_role role, qe_fp8_meta *out_host);
 
-/* Device pointers of the quantized-weight cache and a slot's tape payload.
- * Row strides in bytes are returned in ld_*; any out pointer may be NULL. */
+/* Device pointers of the quantized-weight cache (§3.3) and a slot's tape
+ * payload Q_m (§3.2), for inspection.  Row strides in bytes are returned in
+ * ld_*; any out pointer may be NULL.  Errors: QE_ERR_INVALID_ARG. */
 qe_status qe_layer_cache(const qe_ctx *ctx, int32_t layer, const uint8_t **w_q, int64_t *ld_w_q,
                          const uint8_t **w_q_t, int64_t *ld_w_q_t, const float **w_scale_inv);
 qe_status qe_layer_slot_payload(const qe_ctx *ctx, int32_t layer, int32_t slot, const uint8_t **x_q_t,
@@ -385,8 +400,10 @@ typedef struct {
 } qe_prebuild_desc;
 qe_status qe_prebuild_graphs(qe_ctx *ctx, const qe_prebuild_desc *desc_host);
 
-/* Every bound view written exactly once this epoch (QE_ERR_INCOMPLETE),
- * arena valid (QE_ERR_ARENA_INVALID). */
+/* Arena finalization (§3.4, §4.5; Algorithm 1 before the optimizer step):
+ * every bound view written exactly once this epoch (else QE_ERR_INCOMPLETE,
+ * Table "faults": finalize with a missing dW), arena valid (else
+ * QE_ERR_ARENA_INVALID).  Changes nothing when refused. */
 qe_status qe_arena_finalize(qe_ctx *ctx);
 
 /* Optimizer commit (Algorithm 1, §4.5): requires no live tape
@@ -396,8 +413,11 @@ qe_status qe_arena_finalize(qe_ctx *ctx);
 qe_status qe_optimizer_commit(qe_ctx *ctx);
 
 /* Abort the epoch (§4.5): purge the live tapes of e_W (generations kept) and
- * flag the arena unusable until qe_arena_rebuild. */
+ * flag the arena unusable until qe_arena_rebuild (Table "faults": a write
+ * after an aborted write is refused with QE_ERR_ARENA_INVALID). */
 qe_status qe_abort_epoch(qe_ctx *ctx);
+/* Rebuild the arena after an abort (§4.5): views stay bound, written marks
+ * and finalization are cleared, the arena is valid again. */
 qe_status qe_arena_rebuild(qe_ctx *ctx);
 
 /* Quiescent checkpoint (§3.5, Invariant 4).  A checkpoint holds the
@@ -439,9 +459,11 @@ qe_status qe_checkpoint_export(qe_ctx *ctx, void *buf_host, int64_t capacity, in
 qe_status qe_checkpoint_import(qe_ctx *ctx, const void *buf_host, int64_t size);
 
 /* Block until all device work of the context's actions has finished (the
- * graph stream, and with replay_on_caller the last action's chaining event,
- * which every earlier action precedes), then read back the device effect
- * token. */
+ * graph stream, and the completion event of the last action, which every
+ * earlier action precedes), then read back the device effect token: the
+ * token of §3.2 / Invariant 1, which advances once per F and per dI, so a
+ * caller can check that the device ran exactly the state-mutating actions the
+ * host committed (qe_ctx_state.device_token == .token).  Errors: QE_ERR_HIP. */
 qe_status qe_sync(qe_ctx *ctx);
 
 typedef struct {
@@ -480,16 +502,23 @@ typedef struct {
   const float *view_buf;
 } qe_slot_state;
 
+/* Host snapshots of the contract state (§3.1-§3.6: e_W, the effect token,
+ * arena validity and finalization; per layer e_C and refreshes; per slot
+ * liveness, generation g_p, consumer bits, bound key and view) and of the
+ * executor's counters (graphs, captures, rebinds, replays, handoffs, §4.3 /
+ * §4.4).  Pure reads; no device work.  Errors: QE_ERR_INVALID_ARG. */
 qe_status qe_get_state(const qe_ctx *ctx, qe_ctx_state *out_host);
 qe_status qe_get_layer_state(const qe_ctx *ctx, int32_t layer, qe_layer_state *out_host);
 qe_status qe_get_slot_state(const qe_ctx *ctx, int32_t layer, int32_t slot, qe_slot_state *out_host);
 
-/* Testing hook (host only): the n-th next layer action that passes its checks
- * fails as if its device work could not be enqueued (QE_ERR_HIP; the epoch is
- * aborted).  n = 0 disarms. */
+/* Testing hook (host only), the fault injection of §5.2 and Table "faults"
+ * (a physical failure after the checks): the n-th next layer action that
+ * passes its checks fails as if its device work could not be enqueued
+ * (QE_ERR_HIP; the epoch is aborted, §4.5).  n = 0 disarms. */
 qe_status qe_inject_fault(qe_ctx *ctx, int32_t n);
 
-/* Kernel timing: when enabled (eager mode only), every kernel the context
+/* Kernel timing (measurement support; the paper times whole steps after
+ * warm-up and capture, §5.1): when enabled (eager mode only), every kernel the context
  * launches is bracketed by HIP events on the stream it runs on; totals per kernel
  * class (0 quantize, 1 scale update, 2 GEMM, 3 gradient copy) are read after
  * a qe_sync. */
