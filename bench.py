@@ -695,7 +695,8 @@ def main():
         "quantize": {"achieved": round(q_gbs, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
                      "frac": round(q_gbs / HBM_PEAK_GBS, 4), "avg_launch_us": round(q_ms / q_n * 1e3, 2),
                      "launches": q_n},
-        "scale_update": {"avg_launch_us": round(u_ms / u_n * 1e3, 2), "launches": u_n},
+        "scale_update": ({"avg_launch_us": round(u_ms / u_n * 1e3, 2), "launches": u_n} if u_n else
+                         {"launches": 0, "fused": "runs in extra workgroups of the action's GEMM launch"}),
         "graph": {"graphs_prebuilt": 3 * wl.microbatches * len(wl.linears), "captures": st["captures"],
                   "replays": st["replays"], "rebinds": st["rebinds"], "handoffs": st["handoffs"],
                   "prebuild_ms": round(st["prebuild_ns"] / 1e6, 2), "capture_ms": round(st["capture_ns"] / 1e6, 2)},

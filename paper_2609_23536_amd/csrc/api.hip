@@ -102,6 +102,10 @@ struct Call {
   // FP8 format that runs in the same launch (has_q2 != 0)
   qe::QuantParams q2;
   int32_t has_q2, pad2;
+  // KC_GEMM only: a delayed scale update run by extra workgroups of the same
+  // launch (has_gu != 0)
+  qe::UpdateParams gu;
+  int32_t has_gu, pad3;
   Call() { memset(static_cast<void *>(this), 0, sizeof(*this)); }
 };
 using Plan = std::vector<Call>;
@@ -207,7 +211,7 @@ hipError_t launch(const Call &c, hipStream_t s) {
     case qe::KC_UPDATE: return qe::launch_scale_update(c.u, s);
     case qe::KC_COPY: return qe::launch_grad_copy(c.c, s);
     case qe::KC_AMAX: return qe::launch_amax(c.a, s);
-    default: return qe::launch_gemm(c.g, s);
+    default: return qe::launch_gemm(c.g, s, c.has_gu ? &c.gu : nullptr);
   }
 }
 
@@ -513,6 +517,19 @@ Call update_call(const LayerDev &L, std::initializer_list<int> roles, long long 
   return c;
 }
 
+// Appends a delayed scale update.  Right after a GEMM it rides on the GEMM's
+// launch as extra workgroups: every GEMM of an action reads the scale_inv
+// snapshots of the slot and the weight cache, never the live scales, so the
+// update may run beside it (one launch less per F and per dI).
+void push_update(Plan &p, const Call &u) {
+  if (!p.empty() && p.back().kind == qe::KC_GEMM && !p.back().has_gu) {
+    p.back().gu = u.u;
+    p.back().has_gu = 1;
+  } else {
+    p.push_back(u);
+  }
+}
+
 // Plans of the physical actions (the kernel sequences of §3.2).
 Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt, int64_t tokens, void *y, int y_dt,
               bool refresh) {
@@ -543,7 +560,7 @@ Plan plan_fwd(qe_ctx *c, const LayerDev &L, uint32_t m, const void *x, int x_dt,
     p.push_back(qx);
   p.push_back(gemm_call(L.x_q, d.fmt_x, L.ld_xq, L.w_q, d.fmt_w, L.ld_wq, tokens, d.n_out, d.k_in, S.x_sinv, L.w_sinv,
                         y, y_dt, d.n_out, QE_PLACE_INIT));
-  p.push_back(update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token));
+  push_update(p, update_call(L, {QE_ROLE_X, QE_ROLE_W}, c->d_token));
   return p;
 }
 
@@ -565,7 +582,7 @@ void append_dgrad(qe_ctx *c, Plan &p, const LayerDev &L, uint32_t m, int64_t tok
 }
 
 void finish_dgrad(qe_ctx *c, Plan &p, const LayerDev &L) {
-  if (L.desc.scaling != QE_SCALING_CURRENT) p.push_back(update_call(L, {QE_ROLE_DY}, c->d_token));
+  if (L.desc.scaling != QE_SCALING_CURRENT) push_update(p, update_call(L, {QE_ROLE_DY}, c->d_token));
 }
 
 void append_wgrad(Plan &p, const LayerDev &L, uint32_t m, int64_t tokens, float *mg, int64_t offset, int64_t ld,

@@ -51,6 +51,7 @@
 // Determinism: no atomics and no split reduction; the same inputs produce the
 // same bits, which the split-vs-full-backward check relies on.
 #include "kernels.h"
+#include "scale_update.h"
 
 #include <atomic>
 
@@ -352,7 +353,8 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
 // so its back-edge sits at the barrier, where every LDS read has completed;
 // the waits for fragment reads inside an iteration can then be partial.
 template <int FA, int FB, int OUT, int BM, int BN>
-__global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok) {
+__global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles_m, int tiles_n, int vec_ok,
+                                                         UpdateParams upd) {
   static_assert((BM == 256 || BM == 192) && (BN == 256 || BN == 224 || BN == 192), "tile sizes");
   constexpr int NW = 4, TM = BM / 2, TN = BN / 2;
   constexpr int I = TM / 16, J = TN / 16;    // 16 x 16 MFMA blocks per wave sub-tile
@@ -367,6 +369,17 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
   // two K stages, then one 1 KB block per wave that absorbs the loads issued
   // past the last full K tile (so the loop issues them unconditionally)
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE + NW * 1024];
+  static_assert(sizeof(smem) >= (kMaxHistory + kUpdateThreads / 64) * 4, "history staging fits in the stages");
+
+  // Workgroups past the tiles (dispatched last) run the delayed scale update
+  // of the action's roles beside the tiles: the tiles read the scale_inv
+  // snapshots, never the live scales this update writes.
+  if (int(blockIdx.x) >= tiles_m * tiles_n) {
+    const int r = int(blockIdx.x) - tiles_m * tiles_n;
+    uint32_t *hs = reinterpret_cast<uint32_t *>(smem);
+    scale_update_role(upd.m[r], r == 0 ? upd.token : nullptr, hs, hs + kMaxHistory);
+    return;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -694,24 +707,24 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
 }
 
 template <int FA, int FB, int BM, int BN>
-hipError_t launch_w4(const GemmParams &g, hipStream_t s) {
+hipError_t launch_w4(const GemmParams &g, hipStream_t s, const UpdateParams &u) {
   const int tiles_m = int((g.m + BM - 1) / BM), tiles_n = int((g.n + BN - 1) / BN);
   const uintptr_t cp = reinterpret_cast<uintptr_t>(g.c);
   const int vec_ok = (g.out == 1) ? (g.ldc % 4 == 0 && cp % 8 == 0) : (g.ldc % 4 == 0 && cp % 16 == 0);
-  const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n)), block(256);
+  const dim3 grid(unsigned(tiles_m) * unsigned(tiles_n) + unsigned(u.n)), block(256);
   switch (g.out) {
-    case 0: return klaunch(gemm_tn_w4_kernel<FA, FB, 0, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
-    case 1: return klaunch(gemm_tn_w4_kernel<FA, FB, 1, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
-    default: return klaunch(gemm_tn_w4_kernel<FA, FB, 2, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok);
+    case 0: return klaunch(gemm_tn_w4_kernel<FA, FB, 0, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok, u);
+    case 1: return klaunch(gemm_tn_w4_kernel<FA, FB, 1, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok, u);
+    default: return klaunch(gemm_tn_w4_kernel<FA, FB, 2, BM, BN>, grid, block, 0, s, g, tiles_m, tiles_n, vec_ok, u);
   }
 }
 
 template <int BM, int BN>
-hipError_t launch_w4_fmts(const GemmParams &g, hipStream_t s) {
-  if (g.fmt_a == 0 && g.fmt_b == 0) return launch_w4<0, 0, BM, BN>(g, s);
-  if (g.fmt_a == 1 && g.fmt_b == 0) return launch_w4<1, 0, BM, BN>(g, s);
-  if (g.fmt_a == 0 && g.fmt_b == 1) return launch_w4<0, 1, BM, BN>(g, s);
-  return launch_w4<1, 1, BM, BN>(g, s);
+hipError_t launch_w4_fmts(const GemmParams &g, hipStream_t s, const UpdateParams &u) {
+  if (g.fmt_a == 0 && g.fmt_b == 0) return launch_w4<0, 0, BM, BN>(g, s, u);
+  if (g.fmt_a == 1 && g.fmt_b == 0) return launch_w4<1, 0, BM, BN>(g, s, u);
+  if (g.fmt_a == 0 && g.fmt_b == 1) return launch_w4<0, 1, BM, BN>(g, s, u);
+  return launch_w4<1, 1, BM, BN>(g, s, u);
 }
 
 template <int BM, int BN, int WM, int WN, int FA, int FB>
@@ -763,8 +776,11 @@ static int cu_count() {
   return n;
 }
 
-hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
-  if (g.m <= 0 || g.n <= 0) return hipSuccess;
+hipError_t launch_gemm(const GemmParams &g, hipStream_t s, const UpdateParams *fused) {
+  UpdateParams none;
+  memset(&none, 0, sizeof(none));
+  const UpdateParams &u = fused != nullptr ? *fused : none;
+  if (g.m <= 0 || g.n <= 0) return u.n > 0 ? launch_scale_update(u, s) : hipSuccess;
   // The kernel addresses each operand with 32-bit offsets: split any operand
   // of 2 GiB or more into row blocks (independent GEMMs on disjoint outputs).
   constexpr int64_t kLim = int64_t(1) << 31;
@@ -776,7 +792,7 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
       sub.a = g.a + r * g.lda;
       sub.m = g.m - r < rows ? g.m - r : rows;
       sub.c = static_cast<char *>(g.c) + r * g.ldc * cbytes;
-      const hipError_t e = launch_gemm(sub, s);
+      const hipError_t e = launch_gemm(sub, s, r + rows >= g.m ? fused : nullptr);  // the update rides on the last
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -788,7 +804,7 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
       sub.b = g.b + c0 * g.ldb;
       sub.n = g.n - c0 < cols ? g.n - c0 : cols;
       sub.c = static_cast<char *>(g.c) + c0 * cbytes;
-      const hipError_t e = launch_gemm(sub, s);
+      const hipError_t e = launch_gemm(sub, s, c0 + cols >= g.n ? fused : nullptr);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -809,22 +825,27 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s) {
   const double cn192 = kCost192 * rounds(256, 192);
   const double cm192 = kCost192 * rounds(192, 256);
   const double cn224 = kCost224 * rounds(256, 224);
-  if (force == 1) return launch_w4_fmts<256, 256>(g, s);
-  if (force == 2) return launch_w4_fmts<256, 192>(g, s);
-  if (force == 3) return launch_w4_fmts<192, 256>(g, s);
-  if (force == 4) return launch_fmts<256, 128, 4, 2>(g, s);
-  if (force == 5) return launch_w4_fmts<256, 224>(g, s);
+  // the 8-wave kernel has 512 lanes per workgroup: its update runs as a launch of its own
+  auto eight_wave = [&]() {
+    const hipError_t e = launch_fmts<256, 128, 4, 2>(g, s);
+    return e != hipSuccess || u.n == 0 ? e : launch_scale_update(u, s);
+  };
+  if (force == 1) return launch_w4_fmts<256, 256>(g, s, u);
+  if (force == 2) return launch_w4_fmts<256, 192>(g, s, u);
+  if (force == 3) return launch_w4_fmts<192, 256>(g, s, u);
+  if (force == 4) return eight_wave();
+  if (force == 5) return launch_w4_fmts<256, 224>(g, s, u);
   double best = c256;
   int pick = 1;
   if (cn224 < best) { best = cn224; pick = 5; }
   if (cn192 < best) { best = cn192; pick = 2; }
   if (cm192 < best) { best = cm192; pick = 3; }
   if (c128 < best) { best = c128; pick = 4; }
-  if (pick == 2) return launch_w4_fmts<256, 192>(g, s);
-  if (pick == 3) return launch_w4_fmts<192, 256>(g, s);
-  if (pick == 4) return launch_fmts<256, 128, 4, 2>(g, s);
-  if (pick == 5) return launch_w4_fmts<256, 224>(g, s);
-  return launch_w4_fmts<256, 256>(g, s);
+  if (pick == 2) return launch_w4_fmts<256, 192>(g, s, u);
+  if (pick == 3) return launch_w4_fmts<192, 256>(g, s, u);
+  if (pick == 4) return eight_wave();
+  if (pick == 5) return launch_w4_fmts<256, 224>(g, s, u);
+  return launch_w4_fmts<256, 256>(g, s, u);
 }
 
 void set_gemm_tile_override(int tile) { g_tile_override.store(tile, std::memory_order_relaxed); }

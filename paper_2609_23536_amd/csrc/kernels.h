@@ -165,7 +165,11 @@ hipError_t launch_scale_update(const UpdateParams &p, hipStream_t s);
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 // Two independent casts with the same input dtype and FP8 format in one launch.
 hipError_t launch_quantize_pair(const QuantParams &a, const QuantParams &b, hipStream_t s);
-hipError_t launch_gemm(const GemmParams &p, hipStream_t s);
+// `fused`, if non-null, is a delayed scale update (n >= 1 roles) run in extra
+// workgroups of the same launch (or in a launch of its own right after it when
+// the GEMM is empty or uses the 8-wave kernel); the GEMM must not read the
+// live scales it writes.
+hipError_t launch_gemm(const GemmParams &p, hipStream_t s, const UpdateParams *fused = nullptr);
 // 0: tile shape from the cost model; 1..4: force 256x256, 256x192, 192x256, 256x128
 void set_gemm_tile_override(int tile);
 hipError_t launch_grad_copy(const GradCopyParams &p, hipStream_t s);
