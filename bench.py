@@ -75,6 +75,8 @@ def parse():
                     help="skip the dW-placement measurement at the zero-bubble workload's 2048-token microbatch")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-action latency of the small single-linear schedule")
+    ap.add_argument("--wgrad-only", action="store_true",
+                    help="run only the dW-placement leg (zero-bubble microbatch) and print its JSON")
     ap.add_argument("--no-rotate", action="store_true",
                     help="skip the passes with the caller's buffers rotated every step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -503,6 +505,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.zeros(1, device=dev)
     progress("torch and the library loaded, device initialised")
+    if args.wgrad_only:
+        print(json.dumps({"wgrad_place": wgrad_place(qe, torch, dev)}), flush=True)
+        return
     wl = W.WORKLOADS[args.workload]
     use_graphs = not args.eager
 
