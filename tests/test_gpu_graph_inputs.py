@@ -24,13 +24,19 @@ STEPS = 3
 ROT = 3  # buffer sets rotated over the steps
 
 
-def _run(qe, use_graphs, graph_inputs=0, replay_on_caller=False, rotate=True, prebuild=True):
+def _run(qe, use_graphs, graph_inputs=0, replay_on_caller=False, rotate=True, prebuild=True, current=False,
+         full=False, copy_gradients=False, prebuild_tokens=0):
+    """`full`: dI and dW of each microbatch as one full-backward action (in the dW slots of the
+    schedule, dI slots skipped); `prebuild_tokens`: the token count the graphs are prebuilt for
+    (0: the layers' max_tokens, which is what the calls use)."""
     d = dev()
-    ctx = qe.Context(M, use_graphs=use_graphs, replay_on_caller=replay_on_caller, graph_inputs=graph_inputs)
+    ctx = qe.Context(M, use_graphs=use_graphs, replay_on_caller=replay_on_caller, graph_inputs=graph_inputs,
+                     copy_gradients=copy_gradients)
     L = len(SPEC.shapes)
     ws = [upload(SPEC.weight(u), d) for u in range(L)]
     for u, (n, k) in enumerate(SPEC.shapes):
-        st, idx = ctx.qe_layer_register(0, u, n, k, SPEC.tokens, ws[u], qe.BF16, SPEC.history, SPEC.margin)
+        st, idx = ctx.qe_layer_register(0, u, n, k, SPEC.tokens, ws[u], qe.BF16, 1 if current else SPEC.history,
+                                        SPEC.margin, scaling=qe.SCALING_CURRENT if current else qe.SCALING_DELAYED)
         assert st == "OK" and idx == u
     grad = torch.zeros(SPEC.grad_elems(), dtype=torch.float32, device=d)
     for u, (n, k) in enumerate(SPEC.shapes):
@@ -38,7 +44,7 @@ def _run(qe, use_graphs, graph_inputs=0, replay_on_caller=False, rotate=True, pr
             assert ctx.qe_arena_bind(u, m, grad, grad.numel(), SPEC.offset(u, m), k) == "OK"
     G = 3 * M * L
     if prebuild and use_graphs:
-        assert ctx.qe_prebuild_graphs(0, qe.BF16, qe.F32, qe.BF16, qe.F32) == "OK"
+        assert ctx.qe_prebuild_graphs(prebuild_tokens, qe.BF16, qe.F32, qe.BF16, qe.F32) == "OK"
         st = ctx.qe_get_state()
         assert st["captures"] == G and st["graphs"] == G and st["prebuild_ns"] > 0, st
     t = SPEC.tokens
@@ -65,6 +71,16 @@ def _run(qe, use_graphs, graph_inputs=0, replay_on_caller=False, rotate=True, pr
                     st, refs[(u, m)] = ctx.qe_fp8_linear_fwd(u, key, xb, qe.BF16, t, yb, qe.F32)
                     assert st == "OK", (a, m, u, st)
                     outs[("y", step, u, m)] = yb.clone()
+                elif a == "dI" and full:
+                    continue
+                elif a == "dW" and full:
+                    dyb, dxb = bufs[("dy", u, m)][r], bufs[("dx", u, m)][r]
+                    dyb.copy_(upload(dy, d))
+                    dxb.fill_(float("nan"))
+                    st = ctx.qe_fp8_linear_bwd_full(u, key, refs[(u, m)], dyb, qe.BF16, dxb, qe.F32, grad,
+                                                    SPEC.offset(u, m), k, qe.INIT)
+                    assert st == "OK", (a, m, u, st)
+                    outs[("dx", step, u, m)] = dxb.clone()
                 elif a == "dI":
                     dyb, dxb = bufs[("dy", u, m)][r], bufs[("dx", u, m)][r]
                     dyb.copy_(upload(dy, d))
@@ -142,3 +158,37 @@ def test_recapture_mode_and_no_prebuild():
     lazy = _run(qe, use_graphs=True, prebuild=False)
     _same(ref, lazy)
     assert lazy[2]["captures"] == G  # captured on first use, then rebound
+
+
+@pytest.mark.parametrize("variant", ["current_scaling", "full_backward", "copied_gradients"])
+def test_rotating_buffers_other_plans(variant):
+    """The same rotation on the other kernel sequences an action can have: current
+    scaling (amax pass, update, cast, GEMM), the full backward (dI and dW in one
+    action, with the graphs of its own key captured on first use) and the
+    copied-gradient path (GEMM into the private buffer, then the copy kernel)."""
+    qe = need_lib()
+    kw = {"current": variant == "current_scaling", "full": variant == "full_backward",
+          "copy_gradients": variant == "copied_gradients"}
+    ref = _run(qe, use_graphs=False, **kw)
+    got = _run(qe, use_graphs=True, graph_inputs=qe.GRAPH_INPUTS_REBIND, **kw)
+    _same(ref, got)
+    G = 3 * M * len(SPEC.shapes)
+    if variant == "full_backward":
+        # F graphs prebuilt and rebound; dI / dW graphs prebuilt but unused; one full-backward graph per
+        # (layer, slot) captured on first use and rebound afterwards
+        assert got[2]["captures"] == G + M * len(SPEC.shapes), got[2]
+    else:
+        assert got[2]["captures"] == G, got[2]
+    assert got[2]["rebinds"] > 0
+
+
+def test_prebuilt_for_other_token_count_recaptures_once():
+    """Graphs prebuilt for fewer tokens than the calls use have another launch
+    shape: each is captured again on its first use (bits unchanged), then only
+    rebound."""
+    qe = need_lib()
+    ref = _run(qe, use_graphs=False)
+    got = _run(qe, use_graphs=True, prebuild_tokens=SPEC.tokens - 72)
+    _same(ref, got)
+    G = 3 * M * len(SPEC.shapes)
+    assert G < got[2]["captures"] <= 2 * G, got[2]
