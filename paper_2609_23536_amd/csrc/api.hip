@@ -307,6 +307,9 @@ hipKernelNodeParams node_params(const qe::KernelRec &r, void **argv) {
 // Capture `plan` into e (replacing what e held).
 qe_status capture(qe_ctx *c, GraphEntry &e, const Plan &plan, std::vector<qe::KernelRec> &&recs) {
   const auto t0 = std::chrono::steady_clock::now();
+  // the graph being replaced may still be replaying: let that replay finish
+  // before its executable (and the argument memory it reads) goes away
+  if (e.exec != nullptr && e.launched && hipEventSynchronize(e.done) != hipSuccess) return QE_ERR_HIP;
   if (e.exec != nullptr) (void)hipGraphExecDestroy(e.exec);
   if (e.graph != nullptr) (void)hipGraphDestroy(e.graph);
   e.exec = nullptr;
