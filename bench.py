@@ -55,7 +55,7 @@ METRIC = "FP8 fwd+dI+dW TFLOP/s (% FP8 MFMA peak); quantize/wgrad-place GB/s (% 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100, help="timed steps (the stage replayed 100 times by default)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3_70b_stage_8192tok")
     ap.add_argument("--eager", action="store_true", help="launch kernels directly instead of graph replay")
