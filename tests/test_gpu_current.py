@@ -79,6 +79,26 @@ def test_amax_matches_oracle(dtype, numel, offset, use_accum):
         assert math.isnan(got) if want_nan else got == math.inf
 
 
+@pytest.mark.parametrize("dtype,numel,offset", [("f32", (80 << 20) + 3, 1), ("bf16", (150 << 20) + 5, 7)])
+def test_amax_streamed_tensor_matches_oracle(dtype, numel, offset):
+    """Tensors larger than the 256 MB memory-side cache take the amax pass's
+    non-temporal path: same exact max, NaN still propagates."""
+    qe = need_lib()
+    d = dev()
+    rng = np.random.default_rng(numel)
+    x = rng.standard_normal(numel, dtype=np.float32)
+    x[numel // 3] = -777.25                    # the max in the body
+    buf, addr, vals = _device_tensor(x, dtype, offset, d)
+    assert _amax_via(qe, d, addr, dtype, numel, True) == np.float32(scaling.amax(vals))
+    assert _amax_via(qe, d, addr, dtype, numel, False) == np.float32(scaling.amax(vals))
+    del buf
+    x[numel - 2] = np.nan
+    buf, addr, vals = _device_tensor(x, dtype, offset, d)
+    assert math.isnan(_amax_via(qe, d, addr, dtype, numel, True))
+    del buf
+    torch.cuda.empty_cache()
+
+
 def test_amax_rejects_bad_arguments():
     qe = need_lib()
     d = dev()
