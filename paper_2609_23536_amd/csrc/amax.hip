@@ -16,8 +16,9 @@
 // A tensor that fits in the 256 MB memory-side cache is read with ordinary
 // cached loads (16 per lane in flight), so that the cast that follows re-reads
 // it from that cache; a larger one cannot stay there, and is streamed with
-// non-temporal loads (4 per lane in flight), which read faster on MI355X
-// (measured on a cold 940 MB bf16 tensor: 5.8 TB/s against 3.8 TB/s).  That
+// non-temporal loads (4 per lane in flight, up to 64 workgroups per CU), which
+// read faster on MI355X (measured on a cold 940 MB bf16 tensor: 6.2 TB/s
+// against 3.8 TB/s).  That
 // cache is write-back:
 // when earlier kernels left it dirty, this pass also pays for their write-back
 // to HBM (measured: a cold 235 MB read takes 47 us clean and 100 us right
@@ -32,7 +33,8 @@ constexpr int kThreads = 256;
 constexpr int kUnroll = 16;            // 256 bytes per lane in flight per batch (cached loads)
 constexpr int kUnrollNT = 4;           // 64 bytes (non-temporal loads)
 constexpr int64_t kNTBytes = int64_t(256) << 20;  // the memory-side cache of MI355X
-constexpr int64_t kMaxBlocks = 4096;  // 16 workgroups per CU
+constexpr int64_t kMaxBlocks = 4096;     // cached loads: 16 workgroups per CU
+constexpr int64_t kMaxBlocksNT = 16384;  // non-temporal loads: 64 workgroups per CU
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -106,7 +108,7 @@ hipError_t launch_amax(const AmaxParams &p, hipStream_t s) {
   const bool nt = p.nvec * 16 > kNTBytes;
   const int64_t per = int64_t(kThreads) * (nt ? kUnrollNT : kUnroll);
   int64_t blocks = (p.nvec + per - 1) / per;
-  if (blocks > kMaxBlocks) blocks = kMaxBlocks;
+  if (blocks > (nt ? kMaxBlocksNT : kMaxBlocks)) blocks = nt ? kMaxBlocksNT : kMaxBlocks;
   if (blocks < 1) blocks = 1;
   const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
   if (nt)
