@@ -199,7 +199,9 @@ qe_status qe_quantize_fp8_current_noalloc(const void *in, qe_dtype in_dtype, int
  * (dX = dY W) and dW (dW = dY^T X) of §3.2 are all this call on the codes and
  * transposed codes of qe_quantize_fp8.
  * Layout rules: a, b 16-byte aligned; lda, ldb multiples of 16 and >= k
- * rounded up to 16; ldc >= n; c 4-byte aligned (QE_F32) or 2-byte (QE_BF16).
+ * rounded up to 16; ldc >= n; c 4-byte aligned (QE_F32) or 2-byte (QE_BF16);
+ * k < 2^31.  Operands of 2 GiB or more are run as several launches over
+ * row blocks of A (or of B), with the same per-element results.
  * Errors: QE_ERR_INVALID_ARG; QE_ERR_HIP. */
 qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const uint8_t *b, qe_fp8_fmt fmt_b,
                          int64_t ldb, int64_t m, int64_t n, int64_t k, const float *a_scale_inv,
@@ -303,7 +305,9 @@ void qe_ctx_destroy(qe_ctx *ctx);
  * slot (X_q^T [K, tokens], dY_q^T [N, tokens] and the two scale_inv
  * snapshots: the retained Q_m of §3.2), and scratch for the row-wise X_q /
  * dY_q.  (stage, unit) must be unique (QE_ERR_INVALID_ARG); so must be the
- * bounds: 1 <= history_len <= 8192, formats and dtypes in their enums.
+ * bounds: 1 <= history_len <= 8192, n_out, k_in and max_tokens below 2^31
+ * (each is the reduction length of one of the three products), formats and
+ * dtypes in their enums.
  * With desc->scaling == QE_SCALING_CURRENT every cast below takes its scale
  * from the amax of the tensor it casts (qe_quantize_fp8_current's sequence)
  * instead of from the history; nothing else about the actions changes. */

@@ -841,7 +841,7 @@ qe_status qe_fp8_gemm_tn(const uint8_t *a, qe_fp8_fmt fmt_a, int64_t lda, const 
   if (!valid_fmt(fmt_a) || !valid_fmt(fmt_b) || !valid_dtype(c_dtype)) return QE_ERR_INVALID_ARG;
   if (mode != QE_PLACE_INIT && mode != QE_PLACE_ACCUM) return QE_ERR_INVALID_ARG;
   if (mode == QE_PLACE_ACCUM && c_dtype != QE_F32) return QE_ERR_INVALID_ARG;
-  if (m < 0 || n < 0 || k < 0 || ldc < n) return QE_ERR_INVALID_ARG;
+  if (m < 0 || n < 0 || k < 0 || k >= (int64_t(1) << 31) || ldc < n) return QE_ERR_INVALID_ARG;
   if (m == 0 || n == 0) return QE_OK;
   if (!a || !b || !c || !a_scale_inv || !b_scale_inv) return QE_ERR_INVALID_ARG;
   if (lda % 16 || ldb % 16 || lda < rup16(k) || ldb < rup16(k)) return QE_ERR_INVALID_ARG;
@@ -924,6 +924,8 @@ void qe_ctx_destroy(qe_ctx *c) {
 
 qe_status qe_layer_register(qe_ctx *c, const qe_layer_desc *d, int32_t *layer_out_host) {
   if (c == nullptr || d == nullptr || layer_out_host == nullptr) return QE_ERR_INVALID_ARG;
+  constexpr int64_t kMaxDim = int64_t(1) << 31;  // each is a reduction length of one of the three GEMMs
+  if (d->n_out >= kMaxDim || d->k_in >= kMaxDim || d->max_tokens >= kMaxDim) return QE_ERR_INVALID_ARG;
   if (d->n_out < 1 || d->k_in < 1 || d->max_tokens < 0 || d->history_len < 1 || d->history_len > qe::kMaxHistory ||
       d->margin < -126 || d->margin > 252 || !valid_dtype(d->w_dtype) || !valid_fmt(d->fmt_x) ||
       !valid_fmt(d->fmt_w) || !valid_fmt(d->fmt_dy))

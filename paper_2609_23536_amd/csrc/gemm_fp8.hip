@@ -788,11 +788,19 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s, const UpdateParams *f
   const UpdateParams &u = fused != nullptr ? *fused : none;
   if (g.m <= 0 || g.n <= 0) return u.n > 0 ? launch_scale_update(u, s) : hipSuccess;
   // The kernel addresses each operand with 32-bit offsets: split any operand
-  // of 2 GiB or more into row blocks (independent GEMMs on disjoint outputs).
+  // of 2 GiB or more into row blocks (independent GEMMs on disjoint outputs),
+  // whole 256-row tiles per block where a tile's rows fit in 2 GiB, else as
+  // many rows as fit (at least one: its offsets are then 0 plus the K offset,
+  // which stays below 2^31 because K does).
   constexpr int64_t kLim = int64_t(1) << 31;
+  if (g.k >= kLim) return hipErrorInvalidValue;
+  auto block_rows = [](int64_t ld) -> int64_t {
+    const int64_t r = (kLim - 1) / ld;
+    return r >= 256 ? r / 256 * 256 : (r > 0 ? r : 1);
+  };
   const int64_t cbytes = g.out == 1 ? 2 : 4;
   if (g.m * g.lda >= kLim) {
-    const int64_t rows = (kLim - 1) / g.lda / 256 * 256;
+    const int64_t rows = block_rows(g.lda);
     for (int64_t r = 0; r < g.m; r += rows) {
       GemmParams sub = g;
       sub.a = g.a + r * g.lda;
@@ -804,7 +812,7 @@ hipError_t launch_gemm(const GemmParams &g, hipStream_t s, const UpdateParams *f
     return hipSuccess;
   }
   if (g.n * g.ldb >= kLim) {
-    const int64_t cols = (kLim - 1) / g.ldb / 256 * 256;
+    const int64_t cols = block_rows(g.ldb);
     for (int64_t c0 = 0; c0 < g.n; c0 += cols) {
       GemmParams sub = g;
       sub.b = g.b + c0 * g.ldb;

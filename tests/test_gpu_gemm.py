@@ -241,3 +241,95 @@ def test_tile_shapes_same_bits(forced_tile, shape):
     assert rel_err(outs[0].reshape(m, n), ref) <= 1e-3
     for o in outs[1:]:
         np.testing.assert_array_equal(o, outs[0])
+
+
+def _lut_codes(d, seed, rows, cols, lo, hi, fmt):
+    """Device operands of small integers lo..hi as FP8 codes (exact in either
+    format), drawn on the device; returns (the values as uint8 offsets from lo,
+    on the host, for the reference; the codes, on the device)."""
+    g = torch.Generator(device=d)
+    g.manual_seed(seed)
+    vals = torch.randint(0, hi - lo + 1, (rows, cols), dtype=torch.uint8, device=d, generator=g)
+    lut = torch.from_numpy(fp8.encode(np.arange(lo, hi + 1, dtype=np.float64), fmt)).to(d)
+    codes = lut[vals.int()]
+    return vals.cpu().numpy(), codes
+
+
+def _rows_exact(vals, lo, idx, other_vals, other_lo):
+    """Exact integer products of the sampled rows `idx` of one operand with every row of the other."""
+    a = vals[idx].astype(np.int64) + lo
+    b = other_vals.astype(np.int64) + other_lo
+    return a @ b.T
+
+
+@pytest.mark.parametrize("split", ["rows_of_a", "rows_of_b"])
+def test_operands_of_2gib_split_into_row_blocks(split):
+    """An operand of 2 GiB or more (the kernel's 32-bit offsets) runs as
+    launches over row blocks of whole 256-row tiles: 524,588 rows of 4,096
+    bytes split at row 524,032.  Integer operands, so every output is exact:
+    sampled rows and columns (either side of the split, the ends, random ones)
+    against the integer product, and every column (or row) sum of the output
+    against the sum of the integer operand rows times the other operand.  A
+    split of A stores FP32, then BF16 (the rounding of that exact FP32); a
+    split of B accumulates into an FP32 destination of integers."""
+    qe = need_lib()
+    d = dev()
+    big, small, k = 524_588, 200, 4096
+    assert big * k >= 1 << 31
+    cut = (((1 << 31) - 1) // k) // 256 * 256
+    rng = np.random.default_rng(2031)
+    bv, big_t = _lut_codes(d, 2031, big, k, -6, 6, "E4M3")
+    sv, small_t = _lut_codes(d, 2032, small, k, -6, 6, "E5M2")
+    s = torch.tensor([1.0, 1.0], dtype=torch.float32, device=d)
+    picks = np.unique(np.concatenate([[0, 1, cut - 1, cut, cut + 1, big - 2, big - 1],
+                                      rng.integers(0, big, size=9)]))
+    big_sum = bv.sum(axis=0, dtype=np.int64) - 6 * big        # sum over the big operand's rows
+    sum_ref = (big_sum @ (sv.astype(np.int64) - 6).T)         # per row of the small operand
+    ref_picks = _rows_exact(bv, -6, picks, sv, -6)            # [picks, small]
+    if split == "rows_of_a":
+        m, n = big, small
+        c = torch.empty((m, n), dtype=torch.float32, device=d)
+        assert qe.qe_fp8_gemm_tn(big_t, 0, k, small_t, 1, k, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+        cb = torch.empty((m, n), dtype=torch.int16, device=d)
+        assert qe.qe_fp8_gemm_tn(big_t, 0, k, small_t, 1, k, m, n, k, s[0:1], s[1:2], cb, qe.BF16, n) == "OK"
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(c[torch.from_numpy(picks).to(d)].cpu().numpy(), ref_picks.astype(np.float32))
+        np.testing.assert_array_equal(c.double().sum(dim=0).cpu().numpy(), sum_ref.astype(np.float64))
+        assert torch.equal(cb.view(torch.bfloat16), c.to(torch.bfloat16))
+    else:
+        m, n = small, big
+        base = rng.integers(-50, 50, size=(m, n)).astype(np.float32)
+        c = torch.from_numpy(base).to(d)
+        assert qe.qe_fp8_gemm_tn(small_t, 1, k, big_t, 0, k, m, n, k, s[0:1], s[1:2], c, qe.F32, n,
+                                 qe.ACCUM) == "OK"
+        torch.cuda.synchronize()
+        got = c[:, torch.from_numpy(picks).to(d)].cpu().numpy()
+        np.testing.assert_array_equal(got, (base[:, picks] + ref_picks.T).astype(np.float32))
+        np.testing.assert_array_equal(c.double().sum(dim=1).cpu().numpy(),
+                                      base.astype(np.float64).sum(axis=1) + sum_ref.astype(np.float64))
+
+
+def test_long_reduction_blocks_below_one_tile():
+    """A reduction of 2^23 + 100 bytes per row: a 256-row tile of A would pass
+    2 GiB, so A runs in blocks of 255 rows (then 5), each a partial tile, with a
+    partial last K tile.  Operands in {-1, 0, 1}: every partial sum is an
+    integer of magnitude <= 2^23, so the FP32 result is exact in any order."""
+    qe = need_lib()
+    d = dev()
+    m, n, k = 260, 16, (1 << 23) + 100
+    ld = rup16(k)
+    assert ((1 << 31) - 1) // ld == 255
+    av, a_t = _lut_codes(d, 23, m, ld, -1, 1, "E4M3")
+    bv, b_t = _lut_codes(d, 24, n, ld, -1, 1, "E4M3")
+    a_t[:, k:] = 0x38                             # padding bytes past k (code of 1.0) must be ignored
+    b_t[:, k:] = 0x38
+    s = torch.tensor([1.0, 0.5], dtype=torch.float32, device=d)
+    c = torch.empty((m, n), dtype=torch.float32, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, ld, b_t, 0, ld, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+    torch.cuda.synchronize()
+    got = c.cpu().numpy()
+    # exact: small integers in float32 BLAS (every partial sum an integer below 2^24)
+    b = bv[:, :k].astype(np.float32) - 1.0
+    for r in range(0, m, 32):
+        a = av[r:r + 32, :k].astype(np.float32) - 1.0
+        np.testing.assert_array_equal(got[r:r + 32], (a @ b.T) * np.float32(0.5))

@@ -262,6 +262,18 @@ def test_register_scaling_recipe_validation():
     c.close()
 
 
+def test_register_rejects_reduction_lengths_past_2_31():
+    """n_out, k_in and max_tokens are each the reduction length of one GEMM
+    (dI, F and dW): 2^31 - 1 is accepted, 2^31 is refused."""
+    qe = need_lib()
+    c = qe.Context(1, null_executor=True)
+    big = 1 << 31
+    for u, (n, k, t) in enumerate([(big, 8, 8), (8, big, 8), (8, 8, big)]):
+        assert c.qe_layer_register(0, u, n, k, t, 0, qe.F32, 4, 0)[0] == "INVALID_ARG"
+    assert c.qe_layer_register(0, 0, 8, 8, big - 1, 0, qe.F32, 4, 0) == ("OK", 0)
+    c.close()
+
+
 def test_executor_config_validation():
     """replay_on_caller is 0 or 1, and the one-way (testing) handoff exists only
     for the graph-stream executor."""

@@ -56,6 +56,10 @@ def test_invalid_args_rejected_without_device():
     assert qe.qe_fp8_gemm_tn(16, qe.E4M3, 8, 16, qe.E4M3, 16, 4, 4, 16, 16, 16, 16, qe.F32, 4, stream=0) \
         == "INVALID_ARG"
     assert qe.qe_fp8_gemm_tn(16, 7, 16, 16, qe.E4M3, 16, 4, 4, 16, 16, 16, 16, qe.F32, 4, stream=0) == "INVALID_ARG"
+    # a reduction length of 2^31 or more is refused before any device call
+    k = 1 << 31
+    assert qe.qe_fp8_gemm_tn(16, qe.E4M3, k, 16, qe.E4M3, k, 4, 4, k, 16, 16, 16, qe.F32, 4, stream=0) \
+        == "INVALID_ARG"
     assert qe.qe_amax_scale_update([meta], stream=0) == "INVALID_ARG"
     assert qe.qe_set_gemm_tile(6) == "INVALID_ARG"
     assert qe.qe_set_gemm_tile(-1) == "INVALID_ARG"
