@@ -175,3 +175,64 @@ def test_subnormal_inputs_scaled_to_normal(dtype, fmt, shape):
     qr, qc, _, snap = run_quant(qe, d, t, f, 2.0 ** 126, H=H)
     check(x_f32, fmt, qr, qc, mb1, snap, 2.0 ** 126)
     assert np.count_nonzero(qr) > qr.size // 2
+
+
+def _bf16_rows_f32(bits_i16):
+    """bf16 bit patterns (int16) -> float32 values."""
+    return (bits_i16.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def test_tensor_past_2_31_elements():
+    """A bf16 tensor of 65,613 x 32,808 elements (2^31 plus 5.9 M, 4.3 GB;
+    ragged tiles in both dimensions) through the delayed cast, then through
+    the current-scaling cast (whose amax pass takes the streamed path): the
+    amax of every element against the oracle's (a max over row blocks), sampled
+    rows of the row-wise codes and sampled columns of the transposed codes
+    (first, last and tile-edge indices, random ones) against the oracle's
+    cast, and every transposed code equal to its row-wise one."""
+    qe = need_lib()
+    d = dev()
+    rows, cols = 65_613, 32_808
+    assert rows * cols > 1 << 31
+    g = torch.Generator(device=d)
+    g.manual_seed(31)
+    x = torch.randn((rows, cols), dtype=torch.bfloat16, device=d, generator=g) * 3.0
+    x[rows - 1, cols - 1] = -776.0                     # the largest magnitude, in the last (ragged) tile
+    xh = x.view(torch.int16).cpu().numpy()
+    amax = max(scaling.amax(_bf16_rows_f32(xh[r:r + 4096])) for r in range(0, rows, 4096))
+    assert amax == 776.0
+    rng = np.random.default_rng(31)
+    rpick = np.unique(np.concatenate([[0, 1, 127, 128, 65535, 65536, rows - 1], rng.integers(0, rows, 5)]))
+    cpick = np.unique(np.concatenate([[0, 127, 128, 32767, 32768, cols - 1], rng.integers(0, cols, 5)]))
+    xr = _bf16_rows_f32(xh[rpick])                     # [rpick, cols]
+    xc = _bf16_rows_f32(np.ascontiguousarray(xh[:, cpick].T))  # [cpick, rows]
+    del xh
+    q_row = u8(rows * cols, d)
+    q_col = u8(rows * cols, d)
+
+    def check_codes(scale):
+        np.testing.assert_array_equal(q_row.view(rows, cols)[torch.from_numpy(rpick).to(d)].cpu().numpy(),
+                                      gemm.quantize(xr, scale, "E5M2"))
+        np.testing.assert_array_equal(q_col.view(cols, rows)[torch.from_numpy(cpick).to(d)].cpu().numpy(),
+                                      gemm.quantize(xc, scale, "E5M2"))
+        assert torch.equal(q_row.view(rows, cols).t(), q_col.view(cols, rows))
+
+    # delayed: the meta's scale, the amax recorded into history[0]
+    mb = meta_buffer(4, d, 2.0 ** 4)
+    snap = torch.zeros(1, dtype=torch.float32, device=d)
+    assert qe.qe_quantize_fp8(x, qe.BF16, rows, cols, meta_of(qe, mb, qe.E5M2), q_row, cols, q_col, rows,
+                              snap) == "OK"
+    torch.cuda.synchronize()
+    assert mb[0].item() == amax and snap.item() == 2.0 ** -4
+    check_codes(2.0 ** 4)
+    # current scaling: the scale is set from this tensor's amax first
+    mc = meta_buffer(1, d)
+    token = torch.zeros(1, dtype=torch.int64, device=d)
+    assert qe.qe_quantize_fp8_current(x, qe.BF16, rows, cols, meta_of(qe, mc, qe.E5M2), q_row, cols, q_col, rows,
+                                      snap, token) == "OK"
+    torch.cuda.synchronize()
+    e = scaling.scale_exponent(amax, "E5M2", 0)
+    m = mc.cpu().numpy()
+    assert (m[0], m[1], m[2]) == (0.0, np.float32(2.0 ** e), np.float32(2.0 ** -e))
+    assert snap.item() == 2.0 ** -e and token.item() == 1
+    check_codes(2.0 ** e)
