@@ -522,10 +522,15 @@ qe_status qe_get_slot_state(const qe_ctx *ctx, int32_t layer, int32_t slot, qe_s
 qe_status qe_inject_fault(qe_ctx *ctx, int32_t n);
 
 /* Kernel timing (measurement support; the paper times whole steps after
- * warm-up and capture, §5.1): when enabled (eager mode only), every kernel the context
- * launches is bracketed by HIP events on the stream it runs on; totals per kernel
- * class (0 quantize, 1 scale update, 2 GEMM, 3 gradient copy) are read after
- * a qe_sync. */
+ * warm-up and capture, §5.1): when enabled (eager mode only; replayed graphs
+ * are not bracketed), every launch the context makes is bracketed by HIP
+ * events on the stream it runs on, and counted under its kernel class:
+ * 0 quantize (a paired weight-and-input cast is one launch), 1 stand-alone
+ * scale update, 2 GEMM (with any scale update that runs in its extra
+ * workgroups), 3 gradient copy, 4 amax pass.  qe_get_kernel_timing waits for
+ * the context's actions and returns the running totals of one class since
+ * the context was created (milliseconds, launches); kernel_class outside
+ * 0..4 is QE_ERR_INVALID_ARG. */
 qe_status qe_set_kernel_timing(qe_ctx *ctx, int32_t enable);
 qe_status qe_get_kernel_timing(qe_ctx *ctx, int32_t kernel_class, double *total_ms_host, int64_t *launches_host);
 

@@ -1398,10 +1398,14 @@ qe_status qe_get_kernel_timing(qe_ctx *c, int32_t kernel_class, double *total_ms
   if (!c->cfg.null_executor && !c->timed.empty()) {
     DeviceGuard dg(c->cfg.device);
     if (!dg.ok || sync_actions(c) != hipSuccess) return QE_ERR_HIP;
-    for (auto &t : c->timed) {
-      float ms = 0.f;
-      if (hipEventElapsedTime(&ms, t.t0, t.t1) != hipSuccess) return QE_ERR_HIP;
-      c->kc_ms[t.kind] += ms;
+    // read every pair first, so that a failure leaves the totals and the
+    // pending pairs as they were (a later call reads them again)
+    std::vector<float> ms(c->timed.size(), 0.f);
+    for (size_t i = 0; i < c->timed.size(); ++i)
+      if (hipEventElapsedTime(&ms[i], c->timed[i].t0, c->timed[i].t1) != hipSuccess) return QE_ERR_HIP;
+    for (size_t i = 0; i < c->timed.size(); ++i) {
+      const TimedCall &t = c->timed[i];
+      c->kc_ms[t.kind] += ms[i];
       c->kc_n[t.kind] += 1;
       c->event_pool.push_back(t.t0);
       c->event_pool.push_back(t.t1);

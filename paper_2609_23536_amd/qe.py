@@ -346,8 +346,11 @@ class Context:
         return _st(lib().qe_set_kernel_timing(self.h, int(enable)))
 
     def qe_get_kernel_timing(self, kernel_class: int):
+        """(total milliseconds, launches) of one kernel class; raises on a non-OK status."""
         ms, n = C.c_double(), C.c_int64()
-        _st(lib().qe_get_kernel_timing(self.h, kernel_class, C.byref(ms), C.byref(n)))
+        st = _st(lib().qe_get_kernel_timing(self.h, kernel_class, C.byref(ms), C.byref(n)))
+        if st != "OK":
+            raise RuntimeError(f"qe_get_kernel_timing: {st}")
         return ms.value, n.value
 
     def qe_get_state(self) -> dict:

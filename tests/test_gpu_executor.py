@@ -158,3 +158,64 @@ def test_caller_stream_destroyed_between_actions():
     got = run(True)
     for a, b in zip(ref, got):
         np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("mode", ["delayed", "delayed_copied", "current"])
+def test_kernel_timing_counts_each_class(mode):
+    """Eager kernel timing counts every launch of the actions' kernel
+    sequences (§3.2) under its class.  Per optimizer step, delayed scaling: F
+    (with the weight refresh) is one paired cast and one GEMM whose extra
+    workgroups run the scale update, dI one cast and one GEMM, the deferred dW
+    one GEMM, plus one gradient copy on the copied-gradient path; current
+    scaling adds an amax pass per cast tensor (W, X, dY) and a stand-alone
+    update before each action's casts.  Totals run on across reads; with timing
+    off they stop; an unknown class is refused."""
+    qe = need_lib()
+    d = dev()
+    n, k, t = 256, 320, 160
+    g = torch.Generator(device=d)
+    g.manual_seed(8)
+    w = torch.randn(n, k, device=d, generator=g) * 0.02
+    x = torch.randn(t, k, device=d, generator=g)
+    dy = torch.randn(t, n, device=d, generator=g) * 0.01
+    current = mode == "current"
+    ctx = qe.Context(1, copy_gradients=mode == "delayed_copied")
+    st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.F32, 1 if current else 4, 0,
+                                  scaling=qe.SCALING_CURRENT if current else qe.SCALING_DELAYED)
+    assert st == "OK"
+    grad = torch.zeros(n * k, device=d)
+    assert ctx.qe_arena_bind(L, 0, grad, n * k, 0, k) == "OK"
+    y = torch.zeros(t, n, device=d)
+    dx = torch.zeros(t, k, device=d)
+    classes = (qe.KC_QUANT, qe.KC_UPDATE, qe.KC_GEMM, qe.KC_COPY, qe.KC_AMAX)
+
+    def step(i):
+        key = qe.key(i, 0, 0, 0)
+        st, ref = ctx.qe_fp8_linear_fwd(L, key, x, qe.F32, t, y, qe.F32)
+        assert st == "OK"
+        assert ctx.qe_fp8_linear_dgrad(L, key, ref, dy, qe.F32, dx, qe.F32) == "OK"
+        assert ctx.qe_fp8_linear_wgrad_place(L, key, ref, grad, 0, k, qe.INIT) == "OK"
+        assert ctx.qe_sync() == "OK"
+        assert ctx.qe_arena_finalize() == "OK" and ctx.qe_optimizer_commit() == "OK"
+
+    def counts():
+        return {c: ctx.qe_get_kernel_timing(c) for c in classes}
+
+    per_step = {qe.KC_QUANT: 2, qe.KC_UPDATE: 2 if current else 0, qe.KC_GEMM: 3,
+                qe.KC_COPY: 1 if mode == "delayed_copied" else 0, qe.KC_AMAX: 3 if current else 0}
+    assert all(v == (0.0, 0) for v in counts().values())
+    assert ctx.qe_set_kernel_timing(True) == "OK"
+    step(0)
+    first = counts()
+    step(1)
+    second = counts()
+    for c in classes:
+        assert first[c][1] == per_step[c] and second[c][1] == 2 * per_step[c], (mode, c, first, second)
+        assert (second[c][0] > first[c][0] > 0.0) if per_step[c] else second[c][0] == 0.0
+    assert ctx.qe_set_kernel_timing(False) == "OK"
+    step(2)
+    assert counts() == second
+    for bad in (-1, len(classes)):
+        with pytest.raises(RuntimeError):
+            ctx.qe_get_kernel_timing(bad)
+    ctx.close()
