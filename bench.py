@@ -17,8 +17,9 @@ before timing starts.
 
 Prints one JSON line.  `value` is GEMM FLOPs (fwd + dI + dW, 2*M*N*K each)
 per second over the whole step, quantization and scale updates included.
-`roofline` is the GEMM kernel alone, timed with HIP events on the stream the
-library launches it on, in an instrumented eager pass over the same steps.
+`roofline` is the GEMM kernel alone, timed with HIP events that its launches
+carry on the stream the library launches it on, in an instrumented eager pass
+over the same steps.
 `cpu_baseline` times the CPU oracle stage by stage on a bounded sample of the
 same workload.  Beside the headline the line carries the same steps under the
 other executor, with the actions' kernels launched the other way (direct
@@ -645,7 +646,7 @@ def main():
     progress("dW-placement leg")
     torch.cuda.empty_cache()
 
-    # instrumented eager passes: per-kernel-class times from HIP events on the graph stream
+    # instrumented eager passes: per-kernel-class times from the HIP events the launches carry
     def instrumented(copy_gradients=False, current=False):
         e = StageBench(qe, torch, wl, False, dev, copy_gradients=copy_gradients, current=current)
         e.step()

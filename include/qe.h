@@ -523,8 +523,9 @@ qe_status qe_inject_fault(qe_ctx *ctx, int32_t n);
 
 /* Kernel timing (measurement support; the paper times whole steps after
  * warm-up and capture, §5.1): when enabled (eager mode only; replayed graphs
- * are not bracketed), every launch the context makes is bracketed by HIP
- * events on the stream it runs on, and counted under its kernel class:
+ * are not timed), every launch the context makes is timed by a pair of HIP
+ * events that its kernels carry (hipExtLaunchKernel: from the start of its
+ * first kernel to the end of its last), and counted under its kernel class:
  * 0 quantize (a paired weight-and-input cast is one launch), 1 stand-alone
  * scale update, 2 GEMM (with any scale update that runs in its extra
  * workgroups), 3 gradient copy, 4 amax pass.  qe_get_kernel_timing waits for

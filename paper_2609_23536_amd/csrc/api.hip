@@ -231,12 +231,14 @@ hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed, hipStream_t s) {
     if (timed) {
       TimedCall t{call.kind, pooled_event(c), pooled_event(c)};
       if (!t.t0 || !t.t1) return hipErrorOutOfMemory;
-      hipError_t e = hipEventRecord(t.t0, s);
+      qe::LaunchTiming lt{t.t0, t.t1, false};
+      qe::tl_timing = &lt;
+      hipError_t e = launch(call, s);
+      qe::tl_timing = nullptr;
       if (e != hipSuccess) return e;
-      e = launch(call, s);
-      if (e != hipSuccess) return e;
-      e = hipEventRecord(t.t1, s);
-      if (e != hipSuccess) return e;
+      if (!lt.started) {  // the call launched nothing (an empty tensor): a zero-length pair
+        if ((e = hipEventRecord(t.t0, s)) != hipSuccess || (e = hipEventRecord(t.t1, s)) != hipSuccess) return e;
+      }
       c->timed.push_back(t);
     } else {
       const hipError_t e = launch(call, s);
@@ -258,6 +260,7 @@ hipError_t sync_actions(qe_ctx *c) {
 }  // namespace
 namespace qe {
 thread_local std::vector<KernelRec> *tl_record = nullptr;
+thread_local LaunchTiming *tl_timing = nullptr;
 }
 namespace {
 

@@ -1,6 +1,7 @@
 // Internal launch interface of the gfx950 kernels (not part of the C ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
@@ -42,6 +43,17 @@ struct KernelRec {
 // Installed by the executor on the calling thread while it records a plan.
 extern thread_local std::vector<KernelRec> *tl_record;
 
+// Kernel timing of one executor call, installed on the calling thread while
+// the call launches: the launches carry the events in their own dispatch
+// (hipExtLaunchKernel), so `start` takes the start of the first kernel and
+// `stop` the end of each, i.e. of the last: the pair spans the call's kernels
+// and nothing queued around them.
+struct LaunchTiming {
+  hipEvent_t start, stop;
+  bool started;
+};
+extern thread_local LaunchTiming *tl_timing;
+
 template <typename T>
 inline void pack_arg(KernelRec &r, const T &v) {
   static_assert(sizeof(T) <= 512, "kernel argument too large");
@@ -66,6 +78,11 @@ hipError_t klaunch(void (*f)(P...), dim3 grid, dim3 block, size_t shmem, hipStre
   }
   void *argv[kMaxKernelArgs];
   r.argv(argv);
+  if (tl_timing != nullptr) {
+    hipEvent_t first = tl_timing->started ? nullptr : tl_timing->start;
+    tl_timing->started = true;
+    return hipExtLaunchKernel(r.func, grid, block, argv, shmem, s, first, tl_timing->stop, 0);
+  }
   return hipLaunchKernel(r.func, grid, block, argv, shmem, s);
 }
 
