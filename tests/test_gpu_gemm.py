@@ -333,3 +333,39 @@ def test_long_reduction_blocks_below_one_tile():
     for r in range(0, m, 32):
         a = av[r:r + 32, :k].astype(np.float32) - 1.0
         np.testing.assert_array_equal(got[r:r + 32], (a @ b.T) * np.float32(0.5))
+
+
+# K at and around every count of K tiles the load pipeline treats differently
+# (1 to 9 tiles of 128, full or with a partial last tile), with ragged M and N
+K_EDGE_SHAPES = [(596, 126, 1), (19, 448, 15), (256, 327, 16), (56, 259, 17), (450, 249, 127), (581, 553, 128),
+                 (493, 633, 129), (505, 124, 255), (601, 457, 256), (69, 209, 257), (116, 676, 383),
+                 (509, 643, 384), (198, 445, 385), (423, 527, 640), (83, 361, 897), (451, 578, 1152)]
+
+
+@pytest.mark.parametrize("shape", K_EDGE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_k_tile_counts_exact_every_tile_shape(forced_tile, shape):
+    """Every macro-tile shape at every small count of K tiles (the prologue,
+    the split loads of the K loop, the partial last tile through registers):
+    integer operands, FP32 store and FP32 accumulate exact against the integer
+    product, and the shapes' outputs identical."""
+    qe = forced_tile
+    d = dev()
+    m, n, k = shape
+    ai, bi, a_t, b_t = _int_operands(d, m, n, k, k + 3)
+    lda = a_t.shape[1]
+    ref = (ai.double() @ bi.double().T).float()
+    s = torch.tensor([1.0, 1.0], dtype=torch.float32, device=d)
+    base = torch.randint(-50, 50, (m, n), device=d, generator=torch.Generator(device=d).manual_seed(k)).float()
+    outs = []
+    for tile in (1, 2, 3, 4, 5):
+        assert qe.qe_set_gemm_tile(tile) == "OK"
+        c = torch.empty((m, n), dtype=torch.float32, device=d)
+        assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+        ca = base.clone()
+        assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], ca, qe.F32, n, qe.ACCUM) == "OK"
+        torch.cuda.synchronize()
+        assert torch.equal(c, ref), tile
+        assert torch.equal(ca, base + ref), tile
+        outs.append(c)
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
