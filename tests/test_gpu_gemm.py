@@ -369,3 +369,36 @@ def test_k_tile_counts_exact_every_tile_shape(forced_tile, shape):
         outs.append(c)
     for o in outs[1:]:
         assert torch.equal(o, outs[0])
+
+
+def _sweep_shapes(count, seed):
+    rng = np.random.default_rng(seed)
+    return [(int(rng.integers(1, 1300)), int(rng.integers(1, 1300)), int(rng.integers(1, 2600)))
+            for _ in range(count)]
+
+
+@pytest.mark.parametrize("shape", _sweep_shapes(40, 77), ids=lambda s: "x".join(map(str, s)))
+def test_seeded_shape_sweep_exact(shape):
+    """Forty seeded random shapes (M, N up to 1,300, K up to 2,600) under the
+    automatic tile choice: FP32 store, BF16 store and FP32 accumulate into a
+    padded view, exact on integer operands."""
+    qe = need_lib()
+    d = dev()
+    m, n, k = shape
+    ai, bi, a_t, b_t = _int_operands(d, m, n, k, m + n + k)
+    lda = a_t.shape[1]
+    ref = ai.double() @ bi.double().T
+    s = torch.tensor([1.0, 1.0], dtype=torch.float32, device=d)
+    c = torch.empty((m, n), dtype=torch.float32, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], c, qe.F32, n) == "OK"
+    cb = torch.empty((m, n), dtype=torch.int16, device=d)
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], cb, qe.BF16, n) == "OK"
+    ld = n + 5
+    base = torch.randint(-50, 50, (m, ld), device=d, generator=torch.Generator(device=d).manual_seed(k)).float()
+    ca = base.clone()
+    assert qe.qe_fp8_gemm_tn(a_t, 0, lda, b_t, 0, lda, m, n, k, s[0:1], s[1:2], ca, qe.F32, ld, qe.ACCUM) == "OK"
+    torch.cuda.synchronize()
+    assert torch.equal(c, ref.float())
+    assert torch.equal(cb.view(torch.bfloat16), ref.float().to(torch.bfloat16))
+    assert torch.equal(ca[:, :n], (base[:, :n].double() + ref).float())
+    assert torch.equal(ca[:, n:], base[:, n:])
