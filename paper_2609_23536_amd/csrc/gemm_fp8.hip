@@ -667,6 +667,36 @@ __global__ __launch_bounds__(256) void gemm_tn_w4_kernel(GemmParams g, int tiles
         }
       }
     }
+    if constexpr (OUT == 1) {
+      if (fast) {
+        // BF16 output: rounded before the LDS round trip, which then moves
+        // half the bytes (rows of TN values padded to TN + 8), and every store
+        // instruction writes four 2 * TN-byte row runs, 16 bytes per lane.
+        // The same round-to-nearest-even of the same FP32 value, so the same
+        // bits; measured 0.3-0.5% faster per stage step on MI355X.
+        constexpr int EPH = TN + 8;
+        uint16_t *eh = reinterpret_cast<uint16_t *>(ep);
+        uint16_t *ehw = eh + (lane & 15) * EPH + 4 * (lane >> 4);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int j = 0; j < J; ++j) {
+            const v4f a = acc[2 * i + h][j];
+            *reinterpret_cast<uint2 *>(ehw + h * 16 * EPH + j * 16) =
+                make_uint2(bf16x2_bits(__builtin_ldexpf(a[0], e), __builtin_ldexpf(a[1], e)),
+                           bf16x2_bits(__builtin_ldexpf(a[2], e), __builtin_ldexpf(a[3], e)));
+          }
+        const uint16_t *ehr = eh + (lane >> 4) * EPH + (lane & 15) * 8;
+        const uint32_t voffh = uint32_t((lane >> 4) * g.ldc + (lane & 15) * 8) * 2u;
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          if ((lane & 15) * 8 >= TN) continue;
+          const uint4 v = *reinterpret_cast<const uint4 *>(ehr + it * 4 * EPH);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), crs, voffh, (i * 32 + 4 * it) * rstep, kNT);
+        }
+        continue;
+      }
+    }
     // block rows 2i and 2i+1: lane holds row (lane & 15) of each, four
     // consecutive columns 16 j + 4 (lane >> 4) .. +3 of every column block j
 #pragma unroll
