@@ -24,8 +24,9 @@
 //    where all LDS reads have completed; the compiler can then wait for
 //    fragment reads one by one instead of draining them at the loop head.
 //    The epilogue goes through LDS so every store instruction writes whole
-//    512-byte row runs.  Larger wave tiles mean less LDS traffic per FLOP
-//    than eight waves.
+//    row runs (512-byte FP32 runs; BF16 values are rounded first and go as
+//    256-byte runs).  Larger wave tiles mean less LDS traffic per FLOP than
+//    eight waves.
 //  * gemm_tn_kernel, 256 x 128 x 128 tiles: eight waves (two per SIMD) on a
 //    4 x 2 grid; used when it quantizes better onto the compute units.
 // Operand formats (E4M3 or E5M2) are chosen per call.  K tiles are
