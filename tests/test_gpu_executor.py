@@ -219,3 +219,79 @@ def test_kernel_timing_counts_each_class(mode):
         with pytest.raises(RuntimeError):
             ctx.qe_get_kernel_timing(bad)
     ctx.close()
+
+
+def test_two_contexts_interleaved_match_solo_runs():
+    """Two contexts on one device, their actions interleaved call by call on
+    two caller streams (graph replay, each with its own graph stream, layers
+    and arena): every output equals, bit for bit, the same context's run on
+    its own, so the contexts share no state."""
+    qe = need_lib()
+    d = dev()
+    shapes = [(256, 320, 160), (384, 256, 96)]
+    g = torch.Generator(device=d)
+    g.manual_seed(21)
+    data = []
+    for n, k, t in shapes:
+        w = torch.randn(n, k, device=d, generator=g) * 0.02
+        x = torch.randn(t, k, device=d, generator=g)
+        dy = torch.randn(t, n, device=d, generator=g) * 0.01
+        data.append((n, k, t, w, x, dy))
+
+    def make(i):
+        n, k, t, w, x, dy = data[i]
+        ctx = qe.Context(1, use_graphs=True)
+        st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.F32, 4, 0)
+        assert st == "OK"
+        grad = torch.zeros(n * k, device=d)
+        assert ctx.qe_arena_bind(L, 0, grad, n * k, 0, k) == "OK"
+        return {"ctx": ctx, "L": L, "grad": grad, "y": torch.zeros(t, n, device=d), "dx": torch.zeros(t, k, device=d)}
+
+    def actions(i, s, step):
+        n, k, t, w, x, dy = data[i]
+        key = qe.key(step, 0, 0, 0)
+        c = s["ctx"]
+
+        def fwd():
+            st, s["ref"] = c.qe_fp8_linear_fwd(s["L"], key, x, qe.F32, t, s["y"], qe.F32)
+            return st
+        yield fwd
+        yield lambda: c.qe_fp8_linear_dgrad(s["L"], key, s["ref"], dy, qe.F32, s["dx"], qe.F32)
+        yield lambda: c.qe_fp8_linear_wgrad_place(s["L"], key, s["ref"], s["grad"], 0, k, qe.INIT)
+
+    def finish(s):
+        c = s["ctx"]
+        assert c.qe_sync() == "OK"
+        assert c.qe_arena_finalize() == "OK" and c.qe_optimizer_commit() == "OK"
+
+    def outputs(s):
+        torch.cuda.synchronize()
+        return [s[n].cpu().numpy().copy() for n in ("y", "dx", "grad")]
+
+    solo = []
+    for i in range(2):
+        s = make(i)
+        for step in range(2):
+            for a in actions(i, s, step):
+                assert a() == "OK"
+            finish(s)
+        solo.append(outputs(s))
+        s["ctx"].close()
+
+    both = [make(0), make(1)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()                           # inputs and buffers ready before the side streams run
+    for step in range(2):
+        seqs = [list(actions(i, both[i], step)) for i in range(2)]
+        for a0, a1 in zip(*seqs):
+            with torch.cuda.stream(streams[0]):
+                assert a0() == "OK"
+            with torch.cuda.stream(streams[1]):
+                assert a1() == "OK"
+        for s in both:
+            finish(s)
+    for i in range(2):
+        got = outputs(both[i])
+        for a, b in zip(solo[i], got):
+            np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+        both[i]["ctx"].close()
