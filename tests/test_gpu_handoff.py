@@ -26,9 +26,14 @@ def stale_count(one_way: bool, trials: int, default_stream: bool = False, use_gr
     st, L = ctx.qe_layer_register(0, 0, n, k, t, w, qe.BF16, 4, 0)
     assert st == "OK"
     y = torch.empty((t, n), dtype=torch.bfloat16, device=d)
-    caller = torch.cuda.default_stream(d) if default_stream else torch.cuda.Stream()
+    # The runtime maps streams onto a few hardware queues in turn; a caller
+    # stream that shares the graph stream's queue is serialised with it and
+    # can never see stale data, so the trials cycle over four caller streams
+    # (consecutive ones sit on different queues).
+    callers = [torch.cuda.default_stream(d)] if default_stream else [torch.cuda.Stream() for _ in range(4)]
     stale = 0
     for trial in range(trials):
+        caller = callers[trial % len(callers)]
         with torch.cuda.stream(caller):
             y.fill_(float("nan"))                      # producer's output not written yet
             st, ref = ctx.qe_fp8_linear_fwd(L, qe.key(0, 0, 0, 0), x, qe.BF16, t, y, qe.BF16, caller=caller)
