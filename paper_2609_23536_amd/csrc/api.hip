@@ -235,9 +235,19 @@ hipError_t enqueue(qe_ctx *c, const Plan &plan, bool timed, hipStream_t s) {
       qe::tl_timing = &lt;
       hipError_t e = launch(call, s);
       qe::tl_timing = nullptr;
-      if (e != hipSuccess) return e;
-      if (!lt.started) {  // the call launched nothing (an empty tensor): a zero-length pair
-        if ((e = hipEventRecord(t.t0, s)) != hipSuccess || (e = hipEventRecord(t.t1, s)) != hipSuccess) return e;
+      if (e == hipSuccess && !lt.started) {  // the call launched nothing (an empty tensor): a zero-length pair
+        e = hipEventRecord(t.t0, s);
+        if (e == hipSuccess) e = hipEventRecord(t.t1, s);
+      }
+      if (e != hipSuccess) {
+        if (lt.started) {  // a launch already carries the pair: never hand it out again
+          (void)hipEventDestroy(t.t0);
+          (void)hipEventDestroy(t.t1);
+        } else {           // unused: back to the pool
+          c->event_pool.push_back(t.t0);
+          c->event_pool.push_back(t.t1);
+        }
+        return e;
       }
       c->timed.push_back(t);
     } else {
