@@ -34,9 +34,9 @@
 // (global_load_lds_dwordx4: no register staging, no LDS store instructions)
 // issued a K tile ahead; each wave waits for its own loads and a barrier
 // publishes the stage.  The 4-wave kernel splits a K tile's loads: the B part
-// goes into the stage's B half as soon as every wave holds the previous
-// tile's B fragments (in phase A, a K step and a half before it is read),
-// the A part in the first half of phase B; a second barrier per K step
+// goes into a stage's B half as soon as every wave holds the B fragments of
+// the tile that stage held (during phase A, a K step and a half before it is
+// read), the A part in the first half of phase B; a second barrier per K step
 // marks the B half free.  (Measured on MI355X: against all loads spread over
 // phase B, the Llama-3-70B stage's GEMMs 4% faster, products whose operands
 // stream from HBM up to 8%.)  LDS rows are 128 bytes; their 16-byte chunks are
@@ -353,16 +353,19 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_tn_kernel(GemmParams g, int 
 // A K tile's MFMAs run in two phases of I/2 block rows each:
 //   phase A (block rows 0 .. I/2-1, column-major): uses A fragments
 //     0 .. I/2-1 and every B fragment; reads A fragments I/2 .. I-1 of the
-//     same tile;
+//     same tile; issues the B part of the LDS-bound loads of the tile two K
+//     tiles ahead into this stage's B half;
 //   phase B (block rows I/2 .. I-1, column-major): each B fragment's last use
 //     is followed by the read of the next tile's B fragment into the same
 //     registers, and the next tile's A fragments 0 .. I/2-1 are read too; the
-//     LDS-bound loads of the tile after next are issued.
+//     A part of the loads of the tile after next is issued in its first half.
 // So all of tile t is read by the end of its phase A, where the stage barrier
-// sits: it frees tile t's stage for the loads of tile t+2 and publishes tile
-// t+1, whose loads were issued during the previous phase B (one K tile of
-// latency budget).  Fragment registers: I + J fragments of 8 VGPRs, no second
-// set.  The K loop is rotated (phase B of tile t, then phase A of tile t+1)
+// sits: it frees tile t's A half for the A part of tile t+2 and publishes tile
+// t+1.  A second barrier, after phase B, marks the B half of tile t+1's stage
+// free once every wave holds tile t+1's B fragments, so phase A of tile t+1
+// loads tile t+3's B part there: a K step and a half of latency budget for
+// the B part, about a phase for the A part.  Fragment registers: I + J
+// fragments of 8 VGPRs, no second set.  The K loop is rotated (phase B of tile t, then phase A of tile t+1)
 // so its back-edge sits at the barrier, where every LDS read has completed;
 // the waits for fragment reads inside an iteration can then be partial.
 template <int FA, int FB, int OUT, int BM, int BN>
